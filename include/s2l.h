@@ -1,0 +1,226 @@
+/*
+ * s2l.h - incremental chunked-prefill attention over a paged KV cache, for AMD MI355X (gfx950).
+ *
+ * The operation (Stream2LLM, arXiv 2604.16395):
+ *   - prefill computes a key/value pair for every input token and keeps them as the KV
+ *     cache (Sec. 2.1);
+ *   - the cache is split into fixed blocks of page_size tokens, each placed anywhere in
+ *     memory and found through a per-request block table; attention at position t reads
+ *     every block covering positions 0..t (Sec. 2.2);
+ *   - a streamed request that already holds num_computed_tokens = P cached tokens resumes
+ *     prefill from there (Sec. 4.2): in append mode a newly arrived chunk of C tokens is
+ *     added after them (Sec. 5.1), so its K/V are appended to the pages and its C queries
+ *     attend to the P cached tokens fully and to themselves causally.
+ *   Per scheduler step the engine runs a batch of such requests under a token budget
+ *   (Sec. 4.1); these calls are that step for one attention layer.
+ *
+ * Notation: request r has P_r cached tokens and a chunk of C_r new tokens; T = sum C_r;
+ * Hq query heads, Hkv kv heads, G = Hq / Hkv, head_dim D = 128, page_size S = 16.
+ * Query head h reads kv head h / G.  Chunk token i of request r is absolute position
+ * P_r + i and attends to keys 0 .. P_r + i inclusive.
+ *
+ * Memory and threading contract (all entry points):
+ *   - Every tensor argument is a DEVICE pointer owned by the caller, except the fields
+ *     documented as host pointers.  The library never allocates or frees memory and keeps
+ *     no state between calls; all scratch memory is the caller's workspace.
+ *   - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the null stream).
+ *     Same-stream order is the only ordering: append before attention for the same step.
+ *   - Arguments are validated on the host before anything is enqueued.  On failure the call
+ *     returns a negative s2l_status, enqueues nothing, and s2l_last_error() holds the reason.
+ *     A failed launch returns S2L_EHIP.  Device faults surface at the caller's next sync.
+ *   - Preconditions that are not checked (undefined behaviour if violated): block-table
+ *     entries for the pages a request uses lie in [0, num_pages); device length arrays hold
+ *     the same values as their host copies; pages written by an append belong to that
+ *     request alone (shared prefix pages are read-only); no two in-flight calls share a
+ *     workspace.
+ */
+#ifndef S2L_H
+#define S2L_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define S2L_ABI_VERSION 1
+#define S2L_HEAD_DIM 128
+#define S2L_PAGE_SIZE 16
+
+typedef enum s2l_status {
+  S2L_OK = 0,
+  S2L_EINVAL = -1,     /* a null pointer, negative length or inconsistent argument      */
+  S2L_ERANGE = -2,     /* a request needs more pages than its block-table row holds      */
+  S2L_EWORKSPACE = -3, /* workspace missing or smaller than the plan needs               */
+  S2L_ENOTSUP = -4,    /* unsupported shape: head_dim != 128, page_size != 16, G > 128   */
+  S2L_EHIP = -5        /* a HIP runtime call failed (launch or attribute query)          */
+} s2l_status;
+
+typedef enum s2l_kv_dtype {
+  S2L_KV_BF16 = 0,     /* bf16 elements                                                  */
+  S2L_KV_FP8_E4M3 = 1  /* OCP FP8 E4M3 (e4m3fn) codes with per-kv-head fp32 scales       */
+} s2l_kv_dtype;
+
+/*
+ * One layer's paged KV cache (Sec. 2.2).  K and V are separate pools, each laid out
+ * [num_pages][num_kv_heads][page_size][head_dim]: one (page, kv head) pair is a
+ * contiguous run of page_size * head_dim elements (4 KiB in bf16, 2 KiB in fp8).
+ *
+ * fp8 cache: the stored code of value x of kv head h is e4m3(fp32(x) * fp32(1/scale[h]))
+ * with round-to-nearest-even and saturation to +-448 (NaN stays NaN); the cached value it
+ * stands for is decode(code) * scale[h].  Scales are static, chosen by the caller, > 0.
+ */
+typedef struct s2l_kv_cache {
+  void* k_pages;          /* device; bf16 or uint8 codes                                   */
+  void* v_pages;          /* device; same layout                                           */
+  const float* k_scale;   /* device [num_kv_heads], fp8 only (must be NULL for bf16)       */
+  const float* v_scale;   /* device [num_kv_heads], fp8 only                               */
+  int32_t num_pages;
+  int32_t num_kv_heads;
+  int32_t head_dim;       /* must be 128                                                   */
+  int32_t page_size;      /* must be 16                                                    */
+  int32_t dtype;          /* s2l_kv_dtype                                                  */
+  int32_t reserved;
+} s2l_kv_cache;
+
+/*
+ * One scheduler step's varlen batch (Sec. 4.1: a continuous batch under a token budget).
+ * prefix_lens is num_computed_tokens per request (Sec. 4.2).  chunk_lens may be 0 (the
+ * request is skipped).  Row i of request r in q / k_new / v_new / out is row cu_chunk[r] + i.
+ */
+typedef struct s2l_batch {
+  int32_t num_reqs;                /* R >= 0                                                */
+  int32_t max_pages_per_req;       /* columns of block_tables                               */
+  const int32_t* prefix_lens;      /* device [R]      P_r >= 0                              */
+  const int32_t* chunk_lens;       /* device [R]      C_r >= 0                              */
+  const int32_t* cu_chunk;         /* device [R+1]    exclusive prefix sum of chunk_lens     */
+  const int32_t* block_tables;     /* device [R][max_pages_per_req] physical page ids       */
+  const int32_t* prefix_lens_host; /* HOST [R], same values (validation and grid sizing)   */
+  const int32_t* chunk_lens_host;  /* HOST [R], same values                                 */
+} s2l_batch;
+
+/* Tunables of the work partitioner; pass NULL for the defaults. */
+typedef struct s2l_plan_opts {
+  int32_t target_items;    /* work items wanted before prefixes are split; 0 = 2 x CU count */
+  int32_t min_split_keys;  /* smallest key range of a split piece; 0 = 512 (rounded to 64) */
+  int32_t max_splits;      /* most pieces per request; 0 = 16 (at most 64)                  */
+  int32_t reserved;
+} s2l_plan_opts;
+
+/* What a plan contains, returned to the host by s2l_attn_plan. */
+typedef struct s2l_plan_info {
+  int32_t num_items;       /* attention work items (one workgroup each)                    */
+  int32_t num_split_reqs;  /* requests whose key range is split (they need the reduction)  */
+  int32_t split_keys;      /* target piece length in keys; 0 when nothing is split         */
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t num_reqs;
+  int64_t total_tokens;    /* T                                                             */
+  int64_t workspace_bytes; /* bytes of workspace this plan uses                            */
+} s2l_plan_info;
+
+/* ABI version (S2L_ABI_VERSION of the built library). */
+int32_t s2l_abi_version(void);
+
+/* Reason for the last failure on the calling thread ("" if none); valid until the next
+ * call on this thread. */
+const char* s2l_last_error(void);
+
+/*
+ * Append each request's chunk K/V to its pages (Sec. 2.2 paging; Sec. 4.2 / Sec. 5.1 append).
+ * For i in [0, C_r), h in [0, Hkv): position p = P_r + i goes to page
+ * block_tables[r][p / 16], slot p % 16.  Only those slots are written; every other byte of
+ * the pools is left untouched (a partially filled first page keeps its earlier slots).
+ *   k_new, v_new : device bf16 [T][Hkv][128].
+ * Errors: EINVAL (nulls, negative lengths, fp8 without scales), ERANGE (P_r + C_r >
+ * max_pages_per_req * 16), ENOTSUP (head_dim/page_size), EHIP.
+ */
+s2l_status s2l_kv_append(const s2l_kv_cache* cache, const s2l_batch* batch,
+                         const void* k_new, const void* v_new, void* stream);
+
+/*
+ * Copy stored K/V elements of positions 0..n_r-1 of every request out of the pages,
+ * bit-exact (bf16 bits or fp8 codes, not dequantised); n_r = P_r + C_r if include_chunk,
+ * else P_r.  Request r's rows go to rows cu_out[r] .. cu_out[r] + n_r - 1 of k_out / v_out,
+ * each [rows][Hkv][128] elements of the cache dtype.  For testing and for swap-out.
+ *   cu_out : device int32 [R+1] row offsets chosen by the caller (need not be dense).
+ */
+s2l_status s2l_kv_gather(const s2l_kv_cache* cache, const s2l_batch* batch, int32_t include_chunk,
+                         const int32_t* cu_out, void* k_out, void* v_out, void* stream);
+
+/*
+ * Workspace bytes that s2l_attn_plan and the attention calls need for this batch (host
+ * computation from the host length copies; opts as for s2l_attn_plan).
+ */
+s2l_status s2l_attn_workspace_bytes(const s2l_batch* batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                    const s2l_plan_opts* opts, size_t* bytes_out);
+
+/*
+ * Build the varlen work partition for one step and store it in the workspace (a small
+ * kernel on `stream`); reuse it for every layer of the step.  Each request's chunk is cut
+ * into query tiles of 128 / G tokens x G heads per kv head.  When the batch has fewer than
+ * target_items tiles, each request's key range 0 .. P_r + i_end is split into up to
+ * max_splits pieces of >= min_split_keys keys, so that long prefixes spread over more
+ * workgroups (their partial results are merged by s2l_split_reduce).
+ *   workspace : device, ws_bytes >= s2l_attn_workspace_bytes(...).
+ *   info      : HOST out, describes the plan; pass it to the attention calls.
+ */
+s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t num_kv_heads,
+                         const s2l_plan_opts* opts, void* workspace, size_t ws_bytes,
+                         s2l_plan_info* info, void* stream);
+
+/*
+ * Chunk-prefill attention (Sec. 2.1 prefill over the pages of Sec. 2.2, restarted at
+ * num_computed_tokens as in Sec. 4.2): for request r, chunk row i, query head h,
+ * g = h / G, t = P_r + i:
+ *   s_j = softmax_scale * <q[cu_chunk[r]+i][h], K_r[j][g]>   for j = 0..t
+ *   out[cu_chunk[r]+i][h] = sum_j e^{s_j} V_r[j][g] / sum_j e^{s_j}     (bf16, RNE)
+ *   lse[cu_chunk[r]+i][h] = ln sum_j e^{s_j}                             (fp32, optional)
+ * K_r/V_r are read from the pages after the step's append (the chunk's own keys included;
+ * for an fp8 cache these are its quantised values decode(code) * scale).
+ *   q   : device bf16 [T][Hq][128] (post-RoPE).     out : device bf16 [T][Hq][128].
+ *   lse : device fp32 [T][Hq] or NULL.               softmax_scale > 0 (e.g. 1/sqrt(128)).
+ *   plan: the s2l_plan_info returned by s2l_attn_plan for this batch and head counts.
+ * Equivalent to s2l_attn_main followed by s2l_split_reduce.
+ */
+s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* batch,
+                                  const void* q, int32_t num_q_heads, float softmax_scale,
+                                  void* out, float* lse, const s2l_plan_info* plan,
+                                  void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * The main attention kernel alone (online softmax over the work items of the plan).
+ * Unsplit requests get their final out/lse; split requests get fp32 partials (unnormalised
+ * output, running max, running sum) in the workspace, merged by s2l_split_reduce.
+ */
+s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch,
+                         const void* q, int32_t num_q_heads, float softmax_scale,
+                         void* out, float* lse, const s2l_plan_info* plan,
+                         void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * Log-sum-exp merge of split partials (online-softmax merge): for each row and head of a
+ * split request, m* = max_s m_s, l* = sum_s l_s 2^(m_s - m*), out = sum_s acc_s 2^(m_s - m*) / l*
+ * (bf16), lse = ln(2) (m* + log2 l*).  Enqueues nothing when the plan has no split request.
+ */
+s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* out, float* lse,
+                            const s2l_plan_info* plan, const void* workspace, size_t ws_bytes,
+                            void* stream);
+
+/*
+ * Host-only view of the partition (no GPU needed): fills, for each request, the number of
+ * query tiles and of key-range pieces, and the workspace layout, exactly as s2l_attn_plan
+ * would store them.  items_out, if not NULL, receives num_items rows of 8 int32:
+ * {request, kv_head, token_begin, token_end, key_begin, key_end, piece, num_pieces};
+ * item_capacity is its row count.  num_cus stands in for the device's CU count.
+ */
+s2l_status s2l_plan_host(int32_t num_reqs, const int32_t* prefix_lens_host, const int32_t* chunk_lens_host,
+                         int32_t num_q_heads, int32_t num_kv_heads, const s2l_plan_opts* opts,
+                         int32_t num_cus, s2l_plan_info* info, int32_t* items_out, int64_t item_capacity);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* S2L_H */

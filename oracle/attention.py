@@ -63,7 +63,7 @@ def ref_chunk_attn_loops(q, k, v, P, scale):
     return out, lse
 
 
-def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=None):
+def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=None, with_abs=False):
     """Blocked form of the same definition.
 
     q: [C][Hq][D]; k, v: [>= P+C][Hkv][D] (float64).  ``rows`` optionally selects query
@@ -71,6 +71,9 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
     Pass 1 finds each row's maximum score over all visible keys; pass 2 sums
     exp(s - m) and exp(s - m) V.  Blocks only bound memory: no term is reordered
     beyond summation order.
+
+    ``with_abs`` also returns the same softmax weights applied to |V| (a per-element
+    scale for rounding-error bounds of an implementation that rounds the weights).
     """
     C, hq, d = q.shape
     hkv = k.shape[1]
@@ -78,6 +81,7 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
     rows = np.arange(C) if rows is None else np.asarray(rows, dtype=np.int64)
     n_rows = len(rows)
     out = np.zeros((n_rows, hq, d))
+    out_abs = np.zeros((n_rows, hq, d)) if with_abs else None
     lse = np.zeros((n_rows, hq))
     for g in range(hkv):
         heads = slice(g * g_size, (g + 1) * g_size)
@@ -95,6 +99,7 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
                 m = np.maximum(m, s.max(axis=2))
             den = np.zeros((len(rb), g_size))
             acc = np.zeros((len(rb), g_size, d))
+            acc_abs = np.zeros((len(rb), g_size, d)) if with_abs else None
             for k0 in range(0, kmax, k_block):           # pass 2: sums
                 kb = k[k0:min(kmax, k0 + k_block), g, :]
                 vb = v[k0:min(kmax, k0 + k_block), g, :]
@@ -104,8 +109,14 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
                              np.exp(s - m[:, :, None]), 0.0)
                 den += w.sum(axis=2)
                 acc += np.einsum("ngj,jd->ngd", w, vb)
+                if with_abs:
+                    acc_abs += np.einsum("ngj,jd->ngd", w, np.abs(vb))
             out[b0:b0 + q_block, heads, :] = acc / den[:, :, None]
             lse[b0:b0 + q_block, heads] = m + np.log(den)
+            if with_abs:
+                out_abs[b0:b0 + q_block, heads, :] = acc_abs / den[:, :, None]
+    if with_abs:
+        return out, lse, out_abs
     return out, lse
 
 
@@ -172,17 +183,19 @@ def lse_merge(outs, lses):
 
 def ref_batch_attn(q_rows, k_pool, v_pool, block_tables, prefix_lens, chunk_lens, cu_chunk,
                    num_q_heads, scale, kv_dtype="bf16", k_scale=None, v_scale=None,
-                   sample_rows=None, method="blocked"):
+                   sample_rows=None, method="blocked", with_abs=False):
     """Attention of a varlen batch whose K/V (prefix and chunk) are read through the pools.
 
     q_rows: float64 [T][Hq][D] (the chunk queries, request r at rows cu_chunk[r]..).
     Returns float64 O [T][Hq][D] and LSE [T][Hq] (rows not sampled are NaN when
-    ``sample_rows`` is given as a dict r -> sorted chunk-row indices).
+    ``sample_rows`` is given as a dict r -> sorted chunk-row indices), and with
+    ``with_abs`` the softmax-weighted mean of |V| [T][Hq][D] as a third array.
     """
     T = q_rows.shape[0]
     d = q_rows.shape[2]
     out = np.full((T, num_q_heads, d), np.nan)
     lse = np.full((T, num_q_heads), np.nan)
+    out_abs = np.full((T, num_q_heads, d), np.nan) if with_abs else None
     for r in range(len(prefix_lens)):
         P, C, row0 = int(prefix_lens[r]), int(chunk_lens[r]), int(cu_chunk[r])
         if C == 0:
@@ -195,11 +208,15 @@ def ref_batch_attn(q_rows, k_pool, v_pool, block_tables, prefix_lens, chunk_lens
         v = decode_stored(ref_gather(v_pool, block_tables, r, n), kv_dtype, v_scale)
         q = q_rows[row0:row0 + C]
         if method == "loops":
-            assert rows is None
+            assert rows is None and not with_abs
             o, l = ref_chunk_attn_loops(q, k, v, P, scale)
             out[row0:row0 + C], lse[row0:row0 + C] = o, l
         else:
-            o, l = ref_chunk_attn_blocked(q, k, v, P, scale, rows=rows)
+            res = ref_chunk_attn_blocked(q, k, v, P, scale, rows=rows, with_abs=with_abs)
             idx = np.arange(C) if rows is None else np.asarray(rows)
-            out[row0 + idx], lse[row0 + idx] = o, l
+            out[row0 + idx], lse[row0 + idx] = res[0], res[1]
+            if with_abs:
+                out_abs[row0 + idx] = res[2]
+    if with_abs:
+        return out, lse, out_abs
     return out, lse

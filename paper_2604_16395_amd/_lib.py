@@ -1,0 +1,103 @@
+"""ctypes declarations of the C ABI in include/s2l.h and the loader of libs2l.so.
+
+Loading fails loudly (S2LLibraryMissing) when the built library is absent: there is no
+fallback implementation of any entry point.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libs2l.so")
+
+S2L_OK, S2L_EINVAL, S2L_ERANGE, S2L_EWORKSPACE, S2L_ENOTSUP, S2L_EHIP = 0, -1, -2, -3, -4, -5
+S2L_KV_BF16, S2L_KV_FP8_E4M3 = 0, 1
+STATUS_NAMES = {0: "S2L_OK", -1: "S2L_EINVAL", -2: "S2L_ERANGE", -3: "S2L_EWORKSPACE",
+                -4: "S2L_ENOTSUP", -5: "S2L_EHIP"}
+
+c_i32 = ctypes.c_int32
+c_i64 = ctypes.c_int64
+c_vp = ctypes.c_void_p
+P_i32 = ctypes.POINTER(ctypes.c_int32)
+
+
+class s2l_kv_cache(ctypes.Structure):
+    _fields_ = [("k_pages", c_vp), ("v_pages", c_vp), ("k_scale", c_vp), ("v_scale", c_vp),
+                ("num_pages", c_i32), ("num_kv_heads", c_i32), ("head_dim", c_i32),
+                ("page_size", c_i32), ("dtype", c_i32), ("reserved", c_i32)]
+
+
+class s2l_batch(ctypes.Structure):
+    _fields_ = [("num_reqs", c_i32), ("max_pages_per_req", c_i32), ("prefix_lens", c_vp),
+                ("chunk_lens", c_vp), ("cu_chunk", c_vp), ("block_tables", c_vp),
+                ("prefix_lens_host", P_i32), ("chunk_lens_host", P_i32)]
+
+
+class s2l_plan_opts(ctypes.Structure):
+    _fields_ = [("target_items", c_i32), ("min_split_keys", c_i32), ("max_splits", c_i32),
+                ("reserved", c_i32)]
+
+
+class s2l_plan_info(ctypes.Structure):
+    _fields_ = [("num_items", c_i32), ("num_split_reqs", c_i32), ("split_keys", c_i32),
+                ("num_q_heads", c_i32), ("num_kv_heads", c_i32), ("num_reqs", c_i32),
+                ("total_tokens", c_i64), ("workspace_bytes", c_i64)]
+
+
+P_cache = ctypes.POINTER(s2l_kv_cache)
+P_batch = ctypes.POINTER(s2l_batch)
+P_opts = ctypes.POINTER(s2l_plan_opts)
+P_info = ctypes.POINTER(s2l_plan_info)
+
+# name -> (restype, argtypes); the list of every symbol include/s2l.h declares
+SIGNATURES = {
+    "s2l_abi_version": (c_i32, []),
+    "s2l_last_error": (ctypes.c_char_p, []),
+    "s2l_kv_append": (c_i32, [P_cache, P_batch, c_vp, c_vp, c_vp]),
+    "s2l_kv_gather": (c_i32, [P_cache, P_batch, c_i32, c_vp, c_vp, c_vp, c_vp]),
+    "s2l_attn_workspace_bytes": (c_i32, [P_batch, c_i32, c_i32, P_opts, ctypes.POINTER(ctypes.c_size_t)]),
+    "s2l_attn_plan": (c_i32, [P_batch, c_i32, c_i32, P_opts, c_vp, ctypes.c_size_t, P_info, c_vp]),
+    "s2l_chunk_prefill_attn": (c_i32, [P_cache, P_batch, c_vp, c_i32, ctypes.c_float, c_vp, c_vp, P_info,
+                                       c_vp, ctypes.c_size_t, c_vp]),
+    "s2l_attn_main": (c_i32, [P_cache, P_batch, c_vp, c_i32, ctypes.c_float, c_vp, c_vp, P_info,
+                              c_vp, ctypes.c_size_t, c_vp]),
+    "s2l_split_reduce": (c_i32, [P_batch, c_i32, c_vp, c_vp, P_info, c_vp, ctypes.c_size_t, c_vp]),
+    "s2l_plan_host": (c_i32, [c_i32, P_i32, P_i32, c_i32, c_i32, P_opts, c_i32, P_info, P_i32, c_i64]),
+}
+
+
+class S2LLibraryMissing(ImportError):
+    pass
+
+
+class S2LError(RuntimeError):
+    def __init__(self, fn, status, message):
+        super().__init__(f"{fn} failed: {STATUS_NAMES.get(status, status)}: {message}")
+        self.status = status
+        self.message = message
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libs2l.so (raises S2LLibraryMissing if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise S2LLibraryMissing(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2604_16395_amd.build`")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(handle, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = handle
+    return _lib
+
+
+def call(name, *args):
+    """Call an entry point; raise S2LError on a negative status."""
+    st = getattr(lib(), name)(*args)
+    if st != S2L_OK:
+        raise S2LError(name, st, lib().s2l_last_error().decode())
+    return st

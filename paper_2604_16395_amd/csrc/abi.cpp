@@ -1,0 +1,376 @@
+// C-ABI entry points: host-side validation, the host mirror of the work partition, and
+// kernel launches.  Declarations and the full contract are in include/s2l.h.
+#include "s2l.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "launch.h"
+#include "plan_rules.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+s2l_status fail(s2l_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+s2l_status ok() {
+  g_err.clear();
+  return S2L_OK;
+}
+
+s2l_status hip_fail(const char* what, hipError_t e) {
+  return fail(S2L_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+struct Resolved {
+  int32_t target_items, min_split_keys, max_splits;
+};
+
+s2l_status resolve_opts(const s2l_plan_opts* o, bool need_cus, int32_t num_cus, Resolved* r) {
+  int32_t t = o ? o->target_items : 0, m = o ? o->min_split_keys : 0, x = o ? o->max_splits : 0;
+  if (t < 0 || m < 0 || x < 0) return fail(S2L_EINVAL, "plan opts must be >= 0");
+  if (t == 0) {
+    if (num_cus <= 0 && need_cus) {
+      int dev = 0, n = 0;
+      hipError_t e = hipGetDevice(&dev);
+      if (e == hipSuccess) e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+      if (e != hipSuccess) return hip_fail("querying the CU count", e);
+      num_cus = n;
+    }
+    if (num_cus <= 0) return fail(S2L_EINVAL, "num_cus must be > 0 when target_items is 0");
+    t = s2l::kDefaultItemsPerCu * num_cus;
+  }
+  r->target_items = t;
+  r->min_split_keys = (int32_t)s2l::align_up(m > 0 ? m : s2l::kDefaultMinSplitKeys, s2l::kKvTile);
+  r->max_splits = x > 0 ? (x < s2l::kMaxSplitsCap ? x : s2l::kMaxSplitsCap) : s2l::kDefaultMaxSplits;
+  return S2L_OK;
+}
+
+s2l_status check_heads(int32_t hq, int32_t hkv) {
+  if (hq <= 0 || hkv <= 0) return fail(S2L_EINVAL, "head counts must be > 0 (hq=%d hkv=%d)", hq, hkv);
+  if (hq % hkv != 0) return fail(S2L_EINVAL, "num_q_heads %d is not a multiple of num_kv_heads %d", hq, hkv);
+  if (hq / hkv > s2l::kTileCols)
+    return fail(S2L_ENOTSUP, "query heads per kv head %d exceeds %d", hq / hkv, s2l::kTileCols);
+  return S2L_OK;
+}
+
+// Lengths from the host copies; device pointers checked only when `device` is set.
+s2l_status check_batch(const s2l_batch* b, bool device, int64_t* total_tokens) {
+  if (!b) return fail(S2L_EINVAL, "batch is NULL");
+  if (b->num_reqs < 0) return fail(S2L_EINVAL, "num_reqs %d < 0", b->num_reqs);
+  *total_tokens = 0;
+  if (b->num_reqs == 0) return S2L_OK;
+  if (!b->prefix_lens_host || !b->chunk_lens_host) return fail(S2L_EINVAL, "host length copies are NULL");
+  if (device && (!b->prefix_lens || !b->chunk_lens || !b->cu_chunk || !b->block_tables))
+    return fail(S2L_EINVAL, "a device batch array is NULL");
+  if (device && b->max_pages_per_req <= 0) return fail(S2L_EINVAL, "max_pages_per_req must be > 0");
+  int64_t t = 0;
+  for (int32_t r = 0; r < b->num_reqs; ++r) {
+    const int64_t p = b->prefix_lens_host[r], c = b->chunk_lens_host[r];
+    if (p < 0 || c < 0) return fail(S2L_EINVAL, "request %d: negative length (P=%lld C=%lld)", r, (long long)p, (long long)c);
+    if (p + c > ((int64_t)1 << 30)) return fail(S2L_EINVAL, "request %d: P+C=%lld exceeds 2^30", r, (long long)(p + c));
+    if (device && p + c > (int64_t)b->max_pages_per_req * s2l::kPageSize)
+      return fail(S2L_ERANGE, "request %d: P+C=%lld needs more than max_pages_per_req=%d pages", r,
+                  (long long)(p + c), b->max_pages_per_req);
+    t += c;
+  }
+  if (t >= ((int64_t)1 << 31)) return fail(S2L_EINVAL, "total chunk tokens %lld too large", (long long)t);
+  *total_tokens = t;
+  return S2L_OK;
+}
+
+s2l_status check_cache(const s2l_kv_cache* c, const s2l_batch* b) {
+  if (!c) return fail(S2L_EINVAL, "cache is NULL");
+  if (c->head_dim != s2l::kHeadDim) return fail(S2L_ENOTSUP, "head_dim %d unsupported (only 128)", c->head_dim);
+  if (c->page_size != s2l::kPageSize) return fail(S2L_ENOTSUP, "page_size %d unsupported (only 16)", c->page_size);
+  if (!c->k_pages || !c->v_pages) return fail(S2L_EINVAL, "k_pages/v_pages is NULL");
+  if (c->num_pages <= 0 || c->num_kv_heads <= 0) return fail(S2L_EINVAL, "num_pages and num_kv_heads must be > 0");
+  if (c->dtype == S2L_KV_FP8_E4M3) {
+    if (!c->k_scale || !c->v_scale) return fail(S2L_EINVAL, "fp8 cache needs k_scale and v_scale");
+  } else if (c->dtype == S2L_KV_BF16) {
+    if (c->k_scale || c->v_scale) return fail(S2L_EINVAL, "bf16 cache must pass NULL scales");
+  } else {
+    return fail(S2L_EINVAL, "unknown kv dtype %d", c->dtype);
+  }
+  (void)b;
+  return S2L_OK;
+}
+
+s2l::KvLaunch kv_launch(const s2l_kv_cache* c, const s2l_batch* b) {
+  s2l::KvLaunch a;
+  a.kpool = c->k_pages;
+  a.vpool = c->v_pages;
+  a.kscale = c->k_scale;
+  a.vscale = c->v_scale;
+  a.prefix_lens = b->prefix_lens;
+  a.chunk_lens = b->chunk_lens;
+  a.cu_chunk = b->cu_chunk;
+  a.block_tables = b->block_tables;
+  a.max_pages = b->max_pages_per_req;
+  a.hkv = c->num_kv_heads;
+  a.num_reqs = b->num_reqs;
+  a.fp8 = c->dtype == S2L_KV_FP8_E4M3;
+  return a;
+}
+
+// Host mirror of the device plan kernel (same rules, same order).
+void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_t hkv, const Resolved& o,
+               s2l_plan_info* info, int32_t* items, int64_t cap) {
+  const int32_t g = hq / hkv, tq = s2l::tile_tokens(g);
+  int64_t base = 0, work = 0, tokens = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    base += (int64_t)s2l::num_qtiles(C[r], tq) * hkv;
+    work += s2l::req_work(P[r], C[r], tq) * hkv;
+    tokens += C[r];
+  }
+  const int32_t split_keys = s2l::split_keys_for(base, work, o.target_items, o.min_split_keys);
+  int64_t n_items = 0, part = 0;
+  int32_t n_split = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    const int32_t ns = s2l::req_splits(P[r], C[r], split_keys, o.max_splits);
+    const int32_t nqt = s2l::num_qtiles(C[r], tq);
+    if (items) {
+      for (int32_t gg = 0; gg < hkv; ++gg)
+        for (int32_t qt = 0; qt < nqt; ++qt)
+          for (int32_t s = 0; s < ns; ++s) {
+            const int64_t k = n_items + ((int64_t)gg * nqt + qt) * ns + s;
+            if (k >= cap) continue;
+            const int32_t i0 = qt * tq, i1 = i0 + tq < C[r] ? i0 + tq : C[r];
+            int32_t lo, hi;
+            s2l::piece_range(P[r] + i1, ns, s, &lo, &hi);
+            int32_t* row = items + 8 * k;
+            row[0] = r; row[1] = gg; row[2] = i0; row[3] = i1;
+            row[4] = lo; row[5] = hi; row[6] = s; row[7] = ns;
+          }
+    }
+    n_items += (int64_t)hkv * nqt * ns;
+    part += s2l::req_part_floats(ns, C[r], hq);
+    n_split += ns > 1 ? 1 : 0;
+  }
+  info->num_items = (int32_t)n_items;
+  info->num_split_reqs = n_split;
+  info->split_keys = split_keys;
+  info->num_q_heads = hq;
+  info->num_kv_heads = hkv;
+  info->num_reqs = R;
+  info->total_tokens = tokens;
+  info->workspace_bytes = s2l::workspace_bytes_for(R, part);
+}
+
+s2l_status check_plan(const s2l_plan_info* plan, const s2l_batch* b, int32_t hq, int32_t hkv, int64_t T,
+                      const void* ws, size_t ws_bytes) {
+  if (!plan) return fail(S2L_EINVAL, "plan info is NULL");
+  if (plan->num_q_heads != hq || plan->num_kv_heads != hkv || plan->num_reqs != b->num_reqs ||
+      plan->total_tokens != T)
+    return fail(S2L_EINVAL, "plan was made for another batch or head count");
+  if (!ws) return fail(S2L_EWORKSPACE, "workspace is NULL");
+  if ((int64_t)ws_bytes < plan->workspace_bytes)
+    return fail(S2L_EWORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)plan->workspace_bytes);
+  return S2L_OK;
+}
+
+s2l_status attn_common(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q, int32_t hq,
+                       float scale, void* out, const s2l_plan_info* plan, const void* ws, size_t ws_bytes,
+                       int64_t* T) {
+  s2l_status st;
+  if ((st = check_cache(cache, batch)) != S2L_OK) return st;
+  if ((st = check_batch(batch, true, T)) != S2L_OK) return st;
+  if ((st = check_heads(hq, cache->num_kv_heads)) != S2L_OK) return st;
+  if (!(scale > 0.0f) || !std::isfinite(scale)) return fail(S2L_EINVAL, "softmax_scale must be finite and > 0");
+  if (*T > 0 && (!q || !out)) return fail(S2L_EINVAL, "q/out is NULL");
+  return check_plan(plan, batch, hq, cache->num_kv_heads, *T, ws, ws_bytes);
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t s2l_abi_version(void) { return S2L_ABI_VERSION; }
+
+const char* s2l_last_error(void) { return g_err.c_str(); }
+
+s2l_status s2l_kv_append(const s2l_kv_cache* cache, const s2l_batch* batch, const void* k_new, const void* v_new,
+                         void* stream) {
+  s2l_status st;
+  int64_t T = 0;
+  if ((st = check_cache(cache, batch)) != S2L_OK) return st;
+  if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
+  if (T > 0 && (!k_new || !v_new)) return fail(S2L_EINVAL, "k_new/v_new is NULL");
+  int32_t max_touched = 0;
+  for (int32_t r = 0; r < batch->num_reqs; ++r) {
+    const int32_t p = batch->prefix_lens_host[r], c = batch->chunk_lens_host[r];
+    if (c <= 0) continue;
+    const int32_t n = (p + c - 1) / s2l::kPageSize - p / s2l::kPageSize + 1;
+    if (n > max_touched) max_touched = n;
+  }
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_kv_append(kv_launch(cache, batch), k_new, v_new, max_touched,
+                                       static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("kv_append launch", e);
+  return ok();
+}
+
+s2l_status s2l_kv_gather(const s2l_kv_cache* cache, const s2l_batch* batch, int32_t include_chunk,
+                         const int32_t* cu_out, void* k_out, void* v_out, void* stream) {
+  s2l_status st;
+  int64_t T = 0;
+  if ((st = check_cache(cache, batch)) != S2L_OK) return st;
+  if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
+  if (include_chunk != 0 && include_chunk != 1) return fail(S2L_EINVAL, "include_chunk must be 0 or 1");
+  int32_t max_read = 0;
+  for (int32_t r = 0; r < batch->num_reqs; ++r) {
+    const int32_t n = batch->prefix_lens_host[r] + (include_chunk ? batch->chunk_lens_host[r] : 0);
+    const int32_t pages = (n + s2l::kPageSize - 1) / s2l::kPageSize;
+    if (pages > max_read) max_read = pages;
+  }
+  if (max_read > 0 && (!cu_out || !k_out || !v_out)) return fail(S2L_EINVAL, "cu_out/k_out/v_out is NULL");
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_kv_gather(kv_launch(cache, batch), include_chunk, cu_out, k_out, v_out, max_read,
+                                       static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("kv_gather launch", e);
+  return ok();
+}
+
+s2l_status s2l_attn_workspace_bytes(const s2l_batch* batch, int32_t num_q_heads, int32_t num_kv_heads,
+                                    const s2l_plan_opts* opts, size_t* bytes_out) {
+  s2l_status st;
+  int64_t T = 0;
+  if (!bytes_out) return fail(S2L_EINVAL, "bytes_out is NULL");
+  if ((st = check_batch(batch, false, &T)) != S2L_OK) return st;
+  if ((st = check_heads(num_q_heads, num_kv_heads)) != S2L_OK) return st;
+  Resolved o;
+  if ((st = resolve_opts(opts, true, 0, &o)) != S2L_OK) return st;
+  s2l_plan_info info;
+  host_plan(batch->num_reqs, batch->prefix_lens_host, batch->chunk_lens_host, num_q_heads, num_kv_heads, o, &info,
+            nullptr, 0);
+  *bytes_out = (size_t)info.workspace_bytes;
+  return ok();
+}
+
+s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t num_kv_heads,
+                         const s2l_plan_opts* opts, void* workspace, size_t ws_bytes, s2l_plan_info* info,
+                         void* stream) {
+  s2l_status st;
+  int64_t T = 0;
+  if (!info) return fail(S2L_EINVAL, "info is NULL");
+  if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
+  if (batch->num_reqs > 0 && !batch->cu_chunk) return fail(S2L_EINVAL, "cu_chunk is NULL");
+  if ((st = check_heads(num_q_heads, num_kv_heads)) != S2L_OK) return st;
+  Resolved o;
+  if ((st = resolve_opts(opts, true, 0, &o)) != S2L_OK) return st;
+  s2l_plan_info pi;
+  host_plan(batch->num_reqs, batch->prefix_lens_host, batch->chunk_lens_host, num_q_heads, num_kv_heads, o, &pi,
+            nullptr, 0);
+  if (!workspace) return fail(S2L_EWORKSPACE, "workspace is NULL");
+  if ((int64_t)ws_bytes < pi.workspace_bytes)
+    return fail(S2L_EWORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)pi.workspace_bytes);
+  if (batch->num_reqs == 0 && !batch->cu_chunk) {
+    *info = pi;  // empty batch: nothing for the kernels to read
+    return ok();
+  }
+  s2l::PlanLaunch a;
+  a.prefix_lens = batch->prefix_lens;
+  a.chunk_lens = batch->chunk_lens;
+  a.cu_chunk = batch->cu_chunk;
+  a.num_reqs = batch->num_reqs;
+  a.hq = num_q_heads;
+  a.hkv = num_kv_heads;
+  a.target_items = o.target_items;
+  a.min_split_keys = o.min_split_keys;
+  a.max_splits = o.max_splits;
+  a.ws_bytes = (int64_t)ws_bytes;
+  a.workspace = workspace;
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_attn_plan(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("attn_plan launch", e);
+  *info = pi;
+  return ok();
+}
+
+s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q, int32_t num_q_heads,
+                         float softmax_scale, void* out, float* lse, const s2l_plan_info* plan, void* workspace,
+                         size_t ws_bytes, void* stream) {
+  int64_t T = 0;
+  s2l_status st = attn_common(cache, batch, q, num_q_heads, softmax_scale, out, plan, workspace, ws_bytes, &T);
+  if (st != S2L_OK) return st;
+  s2l::AttnLaunch a;
+  a.kv = kv_launch(cache, batch);
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.hq = num_q_heads;
+  a.softmax_scale = softmax_scale;
+  a.workspace = workspace;
+  a.num_items = plan->num_items;
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("attn_main launch", e);
+  return ok();
+}
+
+s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* out, float* lse,
+                            const s2l_plan_info* plan, const void* workspace, size_t ws_bytes, void* stream) {
+  int64_t T = 0;
+  s2l_status st;
+  if ((st = check_batch(batch, false, &T)) != S2L_OK) return st;
+  if (!plan) return fail(S2L_EINVAL, "plan info is NULL");
+  if ((st = check_plan(plan, batch, num_q_heads, plan->num_kv_heads, T, workspace, ws_bytes)) != S2L_OK) return st;
+  if (plan->num_split_reqs == 0) return ok();
+  if (!out) return fail(S2L_EINVAL, "out is NULL");
+  s2l::ReduceLaunch a;
+  a.out = out;
+  a.lse = lse;
+  a.workspace = workspace;
+  a.hq = num_q_heads;
+  a.num_reqs = batch->num_reqs;
+  a.total_tokens = T;
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_split_reduce(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("split_reduce launch", e);
+  return ok();
+}
+
+s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q,
+                                  int32_t num_q_heads, float softmax_scale, void* out, float* lse,
+                                  const s2l_plan_info* plan, void* workspace, size_t ws_bytes, void* stream) {
+  s2l_status st = s2l_attn_main(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes,
+                                stream);
+  if (st != S2L_OK) return st;
+  return s2l_split_reduce(batch, num_q_heads, out, lse, plan, workspace, ws_bytes, stream);
+}
+
+s2l_status s2l_plan_host(int32_t num_reqs, const int32_t* prefix_lens_host, const int32_t* chunk_lens_host,
+                         int32_t num_q_heads, int32_t num_kv_heads, const s2l_plan_opts* opts, int32_t num_cus,
+                         s2l_plan_info* info, int32_t* items_out, int64_t item_capacity) {
+  s2l_status st;
+  if (!info) return fail(S2L_EINVAL, "info is NULL");
+  s2l_batch b = {};
+  b.num_reqs = num_reqs;
+  b.prefix_lens_host = prefix_lens_host;
+  b.chunk_lens_host = chunk_lens_host;
+  int64_t T = 0;
+  if ((st = check_batch(&b, false, &T)) != S2L_OK) return st;
+  if ((st = check_heads(num_q_heads, num_kv_heads)) != S2L_OK) return st;
+  Resolved o;
+  if ((st = resolve_opts(opts, false, num_cus, &o)) != S2L_OK) return st;
+  if (item_capacity < 0) return fail(S2L_EINVAL, "item_capacity < 0");
+  host_plan(num_reqs, prefix_lens_host, chunk_lens_host, num_q_heads, num_kv_heads, o, info, items_out,
+            item_capacity);
+  return ok();
+}
+
+}  // extern "C"

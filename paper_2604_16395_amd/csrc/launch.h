@@ -1,0 +1,61 @@
+// Internal launcher interface between the C-ABI layer (abi.cpp) and the kernel files.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace s2l {
+
+struct KvLaunch {           // device pointers of one layer's cache and one batch
+  void* kpool;
+  void* vpool;
+  const float* kscale;
+  const float* vscale;
+  const int32_t* prefix_lens;
+  const int32_t* chunk_lens;
+  const int32_t* cu_chunk;
+  const int32_t* block_tables;
+  int32_t max_pages;
+  int32_t hkv;
+  int32_t num_reqs;
+  bool fp8;
+};
+
+hipError_t launch_kv_append(const KvLaunch& a, const void* knew, const void* vnew, int32_t max_pages_touched,
+                            hipStream_t stream);
+hipError_t launch_kv_gather(const KvLaunch& a, int32_t include_chunk, const int32_t* cu_out, void* kout,
+                            void* vout, int32_t max_pages_read, hipStream_t stream);
+
+struct PlanLaunch {
+  const int32_t* prefix_lens;
+  const int32_t* chunk_lens;
+  const int32_t* cu_chunk;
+  int32_t num_reqs, hq, hkv;
+  int32_t target_items, min_split_keys, max_splits;
+  int64_t ws_bytes;
+  void* workspace;
+};
+hipError_t launch_attn_plan(const PlanLaunch& a, hipStream_t stream);
+
+struct AttnLaunch {
+  KvLaunch kv;
+  const void* q;
+  void* out;
+  float* lse;
+  int32_t hq;
+  float softmax_scale;
+  void* workspace;
+  int32_t num_items;        // grid size (host copy of the plan's item count)
+};
+hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream);
+
+struct ReduceLaunch {
+  void* out;
+  float* lse;
+  const void* workspace;
+  int32_t hq;
+  int32_t num_reqs;
+  int64_t total_tokens;
+};
+hipError_t launch_split_reduce(const ReduceLaunch& a, hipStream_t stream);
+
+}  // namespace s2l

@@ -1,0 +1,60 @@
+// Device-side vector types and conversions for gfx950 (CDNA4).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace s2l {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline uint32_t f2u(float x) { return __builtin_bit_cast(uint32_t, x); }
+__device__ inline float u2f(uint32_t x) { return __builtin_bit_cast(float, x); }
+
+// Two fp32 -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ inline uint32_t pack_bf16x2(float a, float b) {
+  f32x2 v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+// Four E4M3 codes (one dword) -> four bf16 (two dwords).  Exact: every E4M3 value is a
+// bf16 value, and the f32 produced by v_cvt_pk_f32_fp8 has a zero low half.
+__device__ inline u32x2 fp8x4_to_bf16x4(uint32_t w) {
+  f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
+  f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(w, true);
+  u32x2 r;
+  r[0] = __builtin_amdgcn_perm(f2u(lo[1]), f2u(lo[0]), 0x07060302u);
+  r[1] = __builtin_amdgcn_perm(f2u(hi[1]), f2u(hi[0]), 0x07060302u);
+  return r;
+}
+
+// Saturate to the finite E4M3 range; NaN passes through (comparisons with NaN are false).
+__device__ inline float sat448(float x) { return x > 448.f ? 448.f : (x < -448.f ? -448.f : x); }
+
+// Four fp32 -> four E4M3 codes (RNE, v_cvt_pk_fp8_f32), after saturation.
+__device__ inline uint32_t f32x4_to_fp8x4(float a, float b, float c, float d) {
+  uint32_t w = 0;
+  w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(sat448(a), sat448(b), (int)w, false);
+  w = (uint32_t)__builtin_amdgcn_cvt_pk_fp8_f32(sat448(c), sat448(d), (int)w, true);
+  return w;
+}
+
+__device__ inline float bf16lo(uint32_t w) { return u2f(w << 16); }
+__device__ inline float bf16hi(uint32_t w) { return u2f(w & 0xFFFF0000u); }
+
+// Exchange with lane l ^ 32 (v_permlane32_swap): r[0], r[1] are {own, partner} in some order.
+__device__ inline float max_with_partner(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(f2u(x), f2u(x), false, false);
+  return fmaxf(u2f(r[0]), u2f(r[1]));
+}
+__device__ inline float sum_with_partner(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(f2u(x), f2u(x), false, false);
+  return u2f(r[0]) + u2f(r[1]);
+}
+
+}  // namespace s2l

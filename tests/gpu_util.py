@@ -1,0 +1,169 @@
+"""Helpers shared by the GPU parity tests: build a case on the device through the C ABI and
+compute the oracle's answer for the same seeded inputs."""
+import math
+
+import numpy as np
+import torch
+
+import paper_2604_16395_amd as s2l
+from oracle.attention import ref_batch_attn
+from oracle.paged_kv import bf16_bits_to_f32, ref_append
+from workloads import BF16_SENTINEL, FP8_SENTINEL
+
+DEV = "cuda"
+SCALE = 1.0 / math.sqrt(128.0)
+
+
+def to_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(DEV).view(torch.bfloat16)
+
+
+def from_bf16(t):
+    return t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def bf16_to_f64(t):
+    return bf16_bits_to_f32(from_bf16(t)).astype(np.float64)
+
+
+def sentinel_pools(case):
+    shape = (case.num_pages, case.num_kv_heads, 16, 128)
+    if case.kv_dtype == "fp8":
+        return np.full(shape, FP8_SENTINEL, np.uint8), np.full(shape, FP8_SENTINEL, np.uint8)
+    return np.full(shape, BF16_SENTINEL, np.uint16), np.full(shape, BF16_SENTINEL, np.uint16)
+
+
+def pool_to_dev(pool):
+    if pool.dtype == np.uint8:
+        return torch.from_numpy(pool).to(DEV)
+    return to_bf16(pool)
+
+
+def pool_from_dev(t):
+    if t.dtype == torch.uint8:
+        return t.cpu().numpy()
+    return from_bf16(t)
+
+
+class Setup:
+    """One step of a case: pools hold each request's prefix (written by the oracle's
+    append), the chunk is appended by the GPU kernel (and by the oracle on its copy)."""
+
+    def __init__(self, case, block_tables=None, prefix_on_gpu=False):
+        self.case = case
+        self.tables = case.block_tables if block_tables is None else block_tables
+        R = case.num_reqs
+        self.kp_ref, self.vp_ref = sentinel_pools(case)
+        zeros = np.zeros(R, np.int32)
+        cu_pre = np.zeros(R + 1, np.int32)
+        cu_pre[1:] = np.cumsum(case.prefix_lens)
+        pre_k, pre_v = case.prefix_rows(case.k_full_bits), case.prefix_rows(case.v_full_bits)
+        self.fp8 = case.kv_dtype == "fp8"
+        self.k_scale = None if not self.fp8 else torch.from_numpy(case.k_scale).to(DEV)
+        self.v_scale = None if not self.fp8 else torch.from_numpy(case.v_scale).to(DEV)
+        if prefix_on_gpu:
+            kd, vd = pool_to_dev(self.kp_ref), pool_to_dev(self.vp_ref)
+            self.cache = s2l.PagedKVCache(kd, vd, self.k_scale, self.v_scale)
+            pb = s2l.Batch(zeros, case.prefix_lens, self.tables)
+            if len(pre_k):
+                s2l.s2l_kv_append(self.cache, pb, to_bf16(pre_k), to_bf16(pre_v))
+        ref_append(self.kp_ref, self.vp_ref, self.tables, zeros, case.prefix_lens, cu_pre, pre_k, pre_v,
+                   case.kv_dtype, case.k_scale, case.v_scale)
+        if not prefix_on_gpu:
+            self.cache = s2l.PagedKVCache(pool_to_dev(self.kp_ref), pool_to_dev(self.vp_ref),
+                                          self.k_scale, self.v_scale)
+        self.batch = s2l.Batch(case.prefix_lens, case.chunk_lens, self.tables)
+        self.k_new = case.new_rows(case.k_full_bits)
+        self.v_new = case.new_rows(case.v_full_bits)
+        self.q = to_bf16(case.q_bits)
+        self.appended = False
+
+    def append(self):
+        s2l.s2l_kv_append(self.cache, self.batch, to_bf16(self.k_new), to_bf16(self.v_new))
+        ref_append(self.kp_ref, self.vp_ref, self.tables, self.case.prefix_lens, self.case.chunk_lens,
+                   self.case.cu_chunk, self.k_new, self.v_new, self.case.kv_dtype, self.case.k_scale,
+                   self.case.v_scale)
+        self.appended = True
+
+    def attention(self, opts=None, with_lse=True, use_main_and_reduce=False):
+        c = self.case
+        T, hq = c.total_tokens, c.num_q_heads
+        nbytes = s2l.s2l_attn_workspace_bytes(self.batch, hq, c.num_kv_heads, opts)
+        ws = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+        plan = s2l.s2l_attn_plan(self.batch, hq, c.num_kv_heads, ws, opts)
+        out = torch.full((T, hq, 128), float("nan"), dtype=torch.bfloat16, device=DEV)
+        lse = torch.full((T, hq), float("nan"), dtype=torch.float32, device=DEV) if with_lse else None
+        if use_main_and_reduce:
+            s2l.s2l_attn_main(self.cache, self.batch, self.q, hq, SCALE, out, lse, plan, ws)
+            s2l.s2l_split_reduce(self.batch, hq, out, lse, plan, ws)
+        else:
+            s2l.s2l_chunk_prefill_attn(self.cache, self.batch, self.q, hq, SCALE, out, lse, plan, ws)
+        torch.cuda.synchronize()
+        self.plan = plan
+        return out, lse
+
+    def oracle(self, sample_rows=None):
+        """(O, LSE, A): the oracle's output, log-sum-exp and softmax-weighted mean of |V|."""
+        c = self.case
+        q = bf16_bits_to_f32(c.q_bits).astype(np.float64)
+        return ref_batch_attn(q, self.kp_ref, self.vp_ref, self.tables, c.prefix_lens, c.chunk_lens,
+                              c.cu_chunk, c.num_q_heads, SCALE, c.kv_dtype, c.k_scale, c.v_scale,
+                              sample_rows=sample_rows, with_abs=True)
+
+
+def sample_rows(case, per_req, rng):
+    """Chunk rows to check per request: first, last, and `per_req` random others."""
+    out = {}
+    for r in range(case.num_reqs):
+        C = int(case.chunk_lens[r])
+        if C == 0:
+            continue
+        pick = {0, C - 1} | set(rng.integers(0, C, size=min(per_req, C)).tolist())
+        out[r] = sorted(pick)
+    return out
+
+
+def assert_attention_close(case, out_gpu, lse_gpu, ref, rows=None, what=""):
+    """Compare bf16 GPU output with the fp64 oracle ``ref`` = (O, LSE, A).
+
+    Error budget of the GPU arithmetic: the probabilities p_j enter the P.V product rounded
+    to bf16 (relative error <= 2^-9 each) while the normaliser sums them in fp32, so the
+    output error is at most 2^-9 sum_j (p_j / l) |V_j| = 2^-9 A; the final bf16 rounding
+    adds 2^-9 |O|; fp32 accumulation adds far less.  Checks (2^-8 leaves a factor 2 of
+    margin over that budget):
+      * max |err| <= 1e-2 (the stated contract);
+      * per element |err| <= 2^-8 (|O| + A) + 1e-6;
+      * per request ||err||_2 / ||O||_2 <= 5e-3 (the budget's typical size is ~2e-3);
+      * |LSE err| <= 1e-4 (1 + |LSE|).
+    """
+    o_ref, l_ref, a_ref = ref
+    o = bf16_to_f64(out_gpu)
+    cu = case.cu_chunk
+    mask = np.zeros(case.total_tokens, dtype=bool)
+    if rows is None:
+        mask[:] = True
+    else:
+        for r, rr in rows.items():
+            mask[cu[r] + np.asarray(rr, dtype=np.int64)] = True
+    a, b = o[mask], o_ref[mask]
+    assert np.isfinite(a).all(), f"{what}: non-finite output"
+    err = np.abs(a - b)
+    assert err.max() <= 1e-2, f"{what}: max abs err {err.max():.3e}"
+    bound = 2.0 ** -8 * (np.abs(b) + a_ref[mask]) + 1e-6
+    bad = err > bound
+    assert not bad.any(), (f"{what}: {bad.sum()} elements over the elementwise bound; worst "
+                           f"excess {(err - bound).max():.3e}, worst err/bound {(err / bound).max():.2f}")
+    for r in range(case.num_reqs):
+        sel = mask[cu[r]:cu[r + 1]]
+        if not sel.any():
+            continue
+        ea = o[cu[r]:cu[r + 1]][sel] - o_ref[cu[r]:cu[r + 1]][sel]
+        rel = np.linalg.norm(ea) / max(np.linalg.norm(o_ref[cu[r]:cu[r + 1]][sel]), 1e-30)
+        assert rel <= 5e-3, f"{what}: request {r} relative L2 err {rel:.3e}"
+    if lse_gpu is not None:
+        lg = lse_gpu.cpu().numpy().astype(np.float64)[mask]
+        lr = l_ref[mask]
+        assert np.isfinite(lg).all()
+        assert (np.abs(lg - lr) <= 1e-4 * (1 + np.abs(lr))).all(), \
+            f"{what}: lse err {np.abs(lg - lr).max():.3e}"
+    return float(err.max())

@@ -1,0 +1,122 @@
+"""GPU: chunk-prefill attention against the fp64 oracle, element by element."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2604_16395_amd as s2l
+import workloads
+from tests.gpu_util import (DEV, SCALE, Setup, assert_attention_close, bf16_to_f64, from_bf16,
+                            sample_rows, to_bf16)
+
+pytestmark = pytest.mark.gpu
+
+FORCE_SPLIT = dict(target_items=1 << 20, min_split_keys=64, max_splits=16)
+
+SMALL = [
+    ("cfg1", [256], [128], 8, 2),
+    ("one_token", [0], [1], 8, 2),
+    ("mha_causal", [0], [200], 8, 8),
+    ("decode_like", [17], [1], 32, 8),
+    ("g3_ragged", [1000], [77], 6, 2),
+    ("varlen", [5, 0, 300, 64, 9], [33, 129, 1, 64, 0], 32, 8),
+    ("g8", [0, 4000], [512, 40], 64, 8),
+    ("page_edges", [15, 16, 17, 31], [1, 16, 15, 33], 8, 2),
+]
+
+
+@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("name,P,C,hq,hkv", SMALL)
+def test_small_cases_match_oracle(name, P, C, hq, hkv, split):
+    case = workloads.make_case(name, P, C, hq, hkv, seed=zlib.crc32(name.encode()) % 1000)
+    print(f"[attn] {name} split={split}", flush=True)
+    s = Setup(case)
+    s.append()
+    out, lse = s.attention(s2l.plan_opts(**FORCE_SPLIT) if split else None)
+    if split and max(P) + max(C) > 64:
+        assert s.plan.num_split_reqs > 0
+    ref = s.oracle()
+    assert_attention_close(case, out, lse, ref, what=name)
+
+
+def test_config1_full_and_first_row_is_v0():
+    case = workloads.config1()
+    s = Setup(case)
+    s.append()
+    out, lse = s.attention()
+    ref = s.oracle()
+    assert_attention_close(case, out, lse, ref, what="cfg1")
+    # P = 0: the first row sees only key 0, so O = V_0 exactly
+    c0 = workloads.make_case("p0", [0], [64], 8, 2, seed=9)
+    s0 = Setup(c0)
+    s0.append()
+    o0, _ = s0.attention()
+    got = from_bf16(o0)[0]                              # [Hq][128]
+    v0 = c0.v_full_bits[0]                              # [Hkv][128]
+    assert np.array_equal(got, np.repeat(v0, 4, axis=0))
+
+
+@pytest.mark.parametrize("q_sigma,k_ramp", [(4.0, 0.0), (4.0, 3.0), (0.5, 6.0)])
+def test_peaky_and_growing_scores(q_sigma, k_ramp):
+    """Score spread of sigma ~2 and keys that grow along the sequence, so the running max
+    rises during the key loop and the rescaling path runs."""
+    case = workloads.make_case("peaky", [3000, 100], [300, 64], 32, 8, seed=10, q_sigma=q_sigma,
+                               k_ramp=k_ramp)
+    for opts in (None, s2l.plan_opts(**FORCE_SPLIT)):
+        s = Setup(case)
+        s.append()
+        out, lse = s.attention(opts)
+        ref = s.oracle()
+        assert_attention_close(case, out, lse, ref, what=f"peaky{q_sigma},{k_ramp}")
+
+
+def test_config2_sampled_rows():
+    case = workloads.config2()
+    s = Setup(case)
+    s.append()
+    out, lse = s.attention()
+    rows = sample_rows(case, 48, np.random.default_rng(2))
+    ref = s.oracle(rows)
+    assert_attention_close(case, out, lse, ref, rows, what="cfg2")
+
+
+def test_config4_mixed_batch_sampled_rows():
+    case = workloads.config4()
+    s = Setup(case)
+    s.append()
+    out, lse = s.attention()
+    rows = sample_rows(case, 4, np.random.default_rng(4))
+    ref = s.oracle(rows)
+    assert_attention_close(case, out, lse, ref, rows, what="cfg4")
+
+
+def test_config5_fp8_cache_sampled_rows():
+    case = workloads.config5()
+    s = Setup(case)
+    s.append()
+    out, lse = s.attention()
+    rows = sample_rows(case, 30, np.random.default_rng(5))
+    ref = s.oracle(rows)
+    assert_attention_close(case, out, lse, ref, rows, what="cfg5")
+
+
+def test_main_plus_reduce_equals_the_combined_call():
+    case = workloads.make_case("mr", [2000], [200], 32, 8, seed=12)
+    s = Setup(case)
+    s.append()
+    a, la = s.attention(s2l.plan_opts(**FORCE_SPLIT))
+    b, lb = s.attention(s2l.plan_opts(**FORCE_SPLIT), use_main_and_reduce=True)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16)) and torch.equal(la, lb)
+
+
+def test_empty_and_zero_length_requests():
+    case = workloads.make_case("zeros", [10, 0, 50], [0, 0, 0], 8, 2, seed=13, pool_pages=8)
+    s = Setup(case)
+    s.append()
+    out, lse = s.attention()
+    assert out.numel() == 0
+    empty = s2l.Batch(np.zeros(0, np.int32), np.zeros(0, np.int32), np.zeros((0, 1), np.int32))
+    ws = torch.empty(s2l.s2l_attn_workspace_bytes(empty, 8, 2), dtype=torch.uint8, device=DEV)
+    plan = s2l.s2l_attn_plan(empty, 8, 2, ws)
+    assert plan.num_items == 0

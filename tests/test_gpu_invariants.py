@@ -1,0 +1,102 @@
+"""GPU: invariants of the attention path (bit-identical where the arithmetic order is
+identical, within tolerance where it is not)."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2604_16395_amd as s2l
+import workloads
+from tests.gpu_util import DEV, SCALE, Setup, assert_attention_close, bf16_to_f64, to_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _eq(a, b):
+    return torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_block_table_permutation_does_not_change_a_bit():
+    a = workloads.make_case("perm", [700, 33], [300, 90], 32, 8, seed=20, table_mode="identity", pool_pages=80)
+    b = workloads.make_case("perm", [700, 33], [300, 90], 32, 8, seed=20, pool_pages=80)
+    assert not np.array_equal(a.block_tables, b.block_tables)
+    outs = []
+    for case in (a, b):
+        s = Setup(case)
+        s.append()
+        outs.append(s.attention()[0])
+    assert _eq(outs[0], outs[1])
+
+
+def test_run_to_run_determinism():
+    case = workloads.make_case("det", [5000, 100], [512, 7], 32, 8, seed=21)
+    s = Setup(case)
+    s.append()
+    for opts in (None, s2l.plan_opts(target_items=1 << 20, min_split_keys=64)):
+        o1, l1 = s.attention(opts)
+        o2, l2 = s.attention(opts)
+        assert _eq(o1, o2) and torch.equal(l1, l2)
+
+
+def test_shared_read_only_prefix_pages_equal_private_copies():
+    P0 = 320                                       # 20 whole pages shared
+    case = workloads.make_case("shared", [P0, P0], [100, 37], 32, 8, seed=22, pool_pages=64)
+    # request 1's prefix = request 0's prefix (same tokens), so the pages may be shared
+    for arr in (case.k_full_bits, case.v_full_bits):
+        arr[case.cu_seq[1]:case.cu_seq[1] + P0] = arr[case.cu_seq[0]:case.cu_seq[0] + P0]
+    private = Setup(case)
+    private.append()
+    o_priv, _ = private.attention()
+    shared_tables = case.block_tables.copy()
+    shared_tables[1, :P0 // 16] = shared_tables[0, :P0 // 16]
+    shared = Setup(case, block_tables=shared_tables)
+    shared.append()
+    o_sh, _ = shared.attention()
+    assert _eq(o_priv, o_sh)
+
+
+def test_split_and_unsplit_agree_within_tolerance():
+    case = workloads.make_case("split", [6000], [256], 32, 8, seed=23)
+    s = Setup(case)
+    s.append()
+    a, la = s.attention(s2l.plan_opts(target_items=1))
+    b, lb = s.attention(s2l.plan_opts(target_items=1 << 20, min_split_keys=64, max_splits=64))
+    assert s.plan.num_split_reqs == 1
+    ref = s.oracle()
+    assert_attention_close(case, a, la, ref, what="unsplit")
+    assert_attention_close(case, b, lb, ref, what="split")
+
+
+def test_streaming_64_chunks_equals_one_shot_prefill():
+    """Config 3: one 32768-token context arriving as 64 chunks of 512; each step appends its
+    K/V and attends over the growing prefix.  The concatenated outputs match the oracle's
+    one-shot causal prefill on sampled rows, and the GPU's own one-shot run everywhere."""
+    case = workloads.config3_stream()
+    kp = torch.full((case.num_pages, 8, 16, 128), 0, dtype=torch.int16, device=DEV)
+    kp.fill_(0x7FBF)
+    vp = kp.clone()
+    cache = s2l.PagedKVCache(kp.view(torch.bfloat16), vp.view(torch.bfloat16))
+    q_all = to_bf16(case.q_bits)
+    k_all = to_bf16(case.k_full_bits)
+    v_all = to_bf16(case.v_full_bits)
+    out = torch.empty((32768, 32, 128), dtype=torch.bfloat16, device=DEV)
+    for step in range(64):
+        P = 512 * step
+        b = s2l.Batch([P], [512], case.block_tables)
+        s2l.s2l_kv_append(cache, b, k_all[P:P + 512].contiguous(), v_all[P:P + 512].contiguous())
+        ws = torch.empty(s2l.s2l_attn_workspace_bytes(b, 32, 8), dtype=torch.uint8, device=DEV)
+        plan = s2l.s2l_attn_plan(b, 32, 8, ws)
+        s2l.s2l_chunk_prefill_attn(cache, b, q_all[P:P + 512].contiguous(), 32, SCALE, out[P:P + 512], None,
+                                   plan, ws)
+    torch.cuda.synchronize()
+    # oracle on sampled rows of the whole sequence (P = 0, C = 32768 view of the same data)
+    s = Setup(case)
+    rng = np.random.default_rng(3)
+    rows = {0: sorted(set(rng.integers(0, 32768, size=160).tolist()) | {0, 511, 512, 32767})}
+    s.append()
+    ref = s.oracle(rows)
+    assert_attention_close(case, out, None, ref, rows, what="stream")
+    # GPU one-shot (P=0, C=32768) vs streamed: both within the bound of each other
+    one, _ = s.attention()
+    a, b = bf16_to_f64(out), bf16_to_f64(one)
+    rms = np.sqrt((b ** 2).mean(axis=-1, keepdims=True))
+    assert (np.abs(a - b) <= 2.0 ** -6 * np.abs(b) + 2.0 ** -7 * rms).all()

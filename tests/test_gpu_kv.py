@@ -1,0 +1,122 @@
+"""GPU: page append and gather are bit-exact against the oracle (whole pools compared)."""
+import numpy as np
+import pytest
+import torch
+
+import paper_2604_16395_amd as s2l
+import workloads
+from oracle.fp8_e4m3 import quantise_kv
+from oracle.paged_kv import bf16_bits_to_f32
+from tests.gpu_util import DEV, Setup, pool_from_dev, to_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_append(case, **kw):
+    print(f"[append] {case.name} dtype={case.kv_dtype}", flush=True)
+    s = Setup(case, **kw)
+    s.append()
+    torch.cuda.synchronize()
+    assert np.array_equal(pool_from_dev(s.cache.k_pages), s.kp_ref), "K pool differs"
+    assert np.array_equal(pool_from_dev(s.cache.v_pages), s.vp_ref), "V pool differs"
+    return s
+
+
+@pytest.mark.parametrize("make", [
+    lambda: workloads.config1(),
+    lambda: workloads.make_case("varlen", [0, 21, 16, 5, 100, 7], [37, 9, 16, 1, 0, 200], 8, 2, seed=3,
+                                pool_pages=40),
+    lambda: workloads.make_case("fp8_varlen", [0, 21, 3], [37, 9, 100], 8, 4, seed=4, kv_dtype="fp8",
+                                pool_pages=20),
+])
+def test_append_is_bit_exact(make):
+    _check_append(make())
+
+
+def test_append_prefix_written_by_the_gpu_matches_too():
+    _check_append(workloads.make_case("gpu_prefix", [300, 40], [50, 0], 8, 2, seed=5, pool_pages=30),
+                  prefix_on_gpu=True)
+
+
+def test_append_config2_and_fp8_config5_shapes():
+    _check_append(workloads.config2())
+    c5 = workloads.make_case("p1000_c2048_h64kv8_fp8", [1000], [2048], 64, 8, seed=1005, kv_dtype="fp8",
+                             pool_pages=200)
+    _check_append(c5)
+
+
+@pytest.mark.parametrize("scale", [1.0, 0.37, 2.0 ** -5])
+def test_fp8_encode_of_every_bf16_pattern(scale):
+    """All 65536 bf16 bit patterns (finite, inf, NaN) through the append kernel's encoder."""
+    case = workloads.make_case("allbits", [0], [512], 8, 1, seed=6, kv_dtype="fp8", pool_pages=32)
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(512, 1, 128)
+    case.k_full_bits[:] = bits
+    case.v_full_bits[:] = bits[::-1]
+    case.k_scale[:] = scale
+    case.v_scale[:] = scale
+    s = Setup(case)
+    s.append()
+    torch.cuda.synchronize()
+    got = pool_from_dev(s.cache.k_pages)
+    ref = s.kp_ref
+    x = bf16_bits_to_f32(bits.reshape(-1))
+    nan = np.isnan(x)
+    # compare slot by slot through the table: positions p -> page table[p // 16], slot p % 16
+    g = np.stack([got[case.block_tables[0][p // 16], 0, p % 16] for p in range(512)]).reshape(-1)
+    r = np.stack([ref[case.block_tables[0][p // 16], 0, p % 16] for p in range(512)]).reshape(-1)
+    assert np.array_equal(g[~nan], r[~nan])
+    assert np.all((g[nan] & 0x7F) == 0x7F)
+    inf = np.isinf(x)
+    assert np.all((g[inf] & 0x7F) == 0x7E)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_gather_round_trip(dtype):
+    case = workloads.make_case("gather", [0, 33, 5], [70, 16, 1], 8, 2, seed=7, kv_dtype=dtype, pool_pages=20)
+    s = Setup(case)
+    s.append()
+    for include in (0, 1):
+        n = case.prefix_lens + (case.chunk_lens if include else 0)
+        cu = np.zeros(case.num_reqs + 1, np.int32)
+        cu[1:] = np.cumsum(n)
+        dt = torch.uint8 if dtype == "fp8" else torch.bfloat16
+        ko = torch.zeros((int(cu[-1]), 2, 128), dtype=dt, device=DEV)
+        vo = torch.zeros_like(ko)
+        s2l.s2l_kv_gather(s.cache, s.batch, include, torch.from_numpy(cu).to(DEV), ko, vo)
+        torch.cuda.synchronize()
+        for r in range(case.num_reqs):
+            rows_k = case.k_full_bits[case.cu_seq[r]:case.cu_seq[r] + n[r]]
+            rows_v = case.v_full_bits[case.cu_seq[r]:case.cu_seq[r] + n[r]]
+            if dtype == "fp8":
+                rows_k = quantise_kv(bf16_bits_to_f32(rows_k), case.k_scale)
+                rows_v = quantise_kv(bf16_bits_to_f32(rows_v), case.v_scale)
+            assert np.array_equal(pool_from_dev(ko)[cu[r]:cu[r + 1]], rows_k)
+            assert np.array_equal(pool_from_dev(vo)[cu[r]:cu[r + 1]], rows_v)
+
+
+def test_swap_out_and_back_in_is_bit_exact():
+    """Pages gathered to host memory and written back (a swap out/in) leave the cache
+    byte-identical, so a resumed request continues exactly."""
+    case = workloads.make_case("swap", [200], [64], 8, 2, seed=8, pool_pages=20)
+    s = Setup(case)
+    s.append()
+    n = np.array([264], np.int32)
+    cu = torch.tensor([0, 264], dtype=torch.int32, device=DEV)
+    ko = torch.empty((264, 2, 128), dtype=torch.bfloat16, device=DEV)
+    vo = torch.empty_like(ko)
+    s2l.s2l_kv_gather(s.cache, s.batch, 1, cu, ko, vo)
+    host_k, host_v = ko.cpu(), vo.cpu()
+    before_k = s.cache.k_pages.clone()
+    s.cache.k_pages.fill_(0)
+    s.cache.v_pages.fill_(0)
+    # swap in: write the saved rows back through the append kernel (P=0, C=264)
+    back = s2l.Batch([0], n, case.block_tables)
+    s2l.s2l_kv_append(s.cache, back, host_k.to(DEV), host_v.to(DEV))
+    torch.cuda.synchronize()
+    full = case.block_tables[0][:16]               # pages 0..15 are full (264 = 16.5 pages)
+    assert torch.equal(s.cache.k_pages[full].view(torch.int16), before_k[full].view(torch.int16))
+    ko2, vo2 = torch.empty_like(ko), torch.empty_like(vo)
+    s2l.s2l_kv_gather(s.cache, back, 1, cu, ko2, vo2)
+    torch.cuda.synchronize()
+    assert torch.equal(ko2.view(torch.int16), ko.view(torch.int16))
+    assert torch.equal(vo2.view(torch.int16), vo.view(torch.int16))

@@ -183,3 +183,13 @@ def test_batch_through_paged_pools_equals_dense_per_request():
                            case.cu_chunk, 4, sc, sample_rows={1: [0, 7], 3: [39]})
     assert np.array_equal(o2[case.cu_chunk[1] + np.array([0, 7])], o[case.cu_chunk[1] + np.array([0, 7])])
     assert np.isnan(o2[0]).all()
+
+
+def test_weighted_abs_values_are_the_same_weights_on_abs_v():
+    rng = np.random.default_rng(8)
+    P, C, d = 30, 9, 16
+    q, k, v = _rand(rng, C, 4, d), _rand(rng, P + C, 2, d), _rand(rng, P + C, 2, d)
+    o, l, oa = ref_chunk_attn_blocked(q, k, v, P, 0.3, k_block=7, with_abs=True)
+    o2, _ = ref_chunk_attn_blocked(q, k, np.abs(v), P, 0.3)
+    assert np.allclose(oa, o2, rtol=1e-13, atol=0)
+    assert np.all(oa >= np.abs(o) - 1e-15)

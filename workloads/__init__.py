@@ -170,16 +170,24 @@ def config1(seed=1001):
     return make_case("p256_c128_h8kv2", [256], [128], 8, 2, seed, pool_pages=64)
 
 
-def config2(seed=1002):
-    """Llama-3-8B layer shape: 8 requests, P ~ U{0..8192}, C = 512; 32q/8kv; 4096-page pool."""
+def config2_lengths(seed=1002):
+    """(P, C, seed actually used): P ~ U{0..8192}, C = 512, re-drawn with seed+1 until the
+    8 requests fit the 4096-page pool."""
     s = seed
     while True:
         rng = np.random.default_rng(s)
         P = rng.integers(0, 8193, size=8)
         C = np.full(8, 512)
         if int(((P + C + 15) // 16).sum()) <= 4096:
-            break
+            return P, C, s
         s += 1
+
+
+def config2(seed=1002):
+    """Llama-3-8B layer shape: 8 requests, P ~ U{0..8192}, C = 512; 32q/8kv; 4096-page pool."""
+    P, C, s = config2_lengths(seed)
+    rng = np.random.default_rng(s)
+    rng.integers(0, 8193, size=8)            # replay the length draw, then Q/K/V follow
     return make_case("batch8_c512_pU8k_h32kv8", P, C, 32, 8, s, pool_pages=4096, rng=rng)
 
 
@@ -198,11 +206,18 @@ def config3_step(step=16, seed=1003):
                      pool_pages=2048)
 
 
-def config4(seed=1004):
-    """Mixed batch: 64 requests, P ~ U{0..32768}, C = clip(floor(lognormal(ln 64, 4.118)), 1, 2048)."""
+def config4_lengths(seed=1004):
+    """P ~ U{0..32768}; C = clip(floor(exp(N(ln 64, 4.118^2))), 1, 2048) (about 20% of rows
+    at C = 1 and 20% at 2048)."""
     rng = np.random.default_rng(seed)
     P = rng.integers(0, 32769, size=64)
     C = np.clip(np.floor(np.exp(rng.normal(np.log(64.0), 4.118, size=64))), 1, 2048).astype(np.int64)
+    return P, C, rng
+
+
+def config4(seed=1004):
+    """Mixed batch: 64 requests, prefixes uniform in [0, 32768], log-normal chunk lengths."""
+    P, C, rng = config4_lengths(seed)
     pages = int(((P + C + 15) // 16).sum())
     return make_case("mixed64_pU32k_clognormal_h32kv8", P, C, 32, 8, seed,
                      pool_pages=int(pages * 1.25), rng=rng)
