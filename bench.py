@@ -1,0 +1,242 @@
+"""Benchmark of the chunked-prefill attention hot path on one MI355X.
+
+Workload (the headline configuration): one request holding an 8192-token cached prefix
+receives a 512-token chunk; Llama-3-8B attention-layer shape (32 query heads, 8 kv heads,
+head dim 128), bf16, 16-token pages, shuffled block table.  One step = the whole path for
+one layer: page append of the chunk's K/V, the work partition, the attention kernel and the
+split-KV merge.  The KV pool is rotated over 32 layer copies so that each step reads its
+pages from HBM rather than from the 256 MB last-level cache, as a 32-layer model would.
+
+Prints ONE JSON line.  `value` is algorithmic TFLOP/s of the whole step (4*d*Hq FLOPs per
+query/visible-key pair, unmasked pairs only) with every input already resident in HBM.
+`roofline` reports the attention kernel alone, timed with HIP events on its own stream.
+`cpu_baseline` times the fp64 oracle on this machine's host cores.
+"""
+import argparse
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0           # MI355X HBM3E
+PROFILE_SUMMARY = os.path.join(ROOT, "profiles", "attn_main_p8192_c512_h32kv8_counters.md")
+KERNEL_SOURCES = ["paper_2604_16395_amd/csrc/chunk_attn.hip", "paper_2604_16395_amd/csrc/s2l_device.h",
+                  "paper_2604_16395_amd/csrc/plan_rules.h"]
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, p), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profile(src_hash):
+    """HBM bytes per launch of the attention kernel from the committed counter summary, or
+    None when there is none or it was taken on another version of the kernel source."""
+    if not os.path.exists(PROFILE_SUMMARY):
+        return None
+    text = open(PROFILE_SUMMARY).read()
+    m_hash = re.search(r"kernel_source_sha256_16:\s*([0-9a-f]+)", text)
+    m_bytes = re.search(r"hbm_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not m_hash or not m_bytes or m_hash.group(1) != src_hash:
+        return None
+    return float(m_bytes.group(1))
+
+
+def cpu_baseline(case, min_seconds=10.0, max_reps=5):
+    """The fp64 oracle on the whole workload (all 512 rows x 32 heads), repeated until at
+    least `min_seconds` have elapsed."""
+    from oracle.attention import ref_batch_attn
+    from oracle.paged_kv import bf16_bits_to_f32, ref_append
+    import workloads
+    R = case.num_reqs
+    shape = (case.num_pages, case.num_kv_heads, 16, 128)
+    kp = np.full(shape, workloads.BF16_SENTINEL, np.uint16)
+    vp = np.full(shape, workloads.BF16_SENTINEL, np.uint16)
+    seq = (case.prefix_lens + case.chunk_lens).astype(np.int32)
+    cu = np.zeros(R + 1, np.int32)
+    cu[1:] = np.cumsum(seq)
+    ref_append(kp, vp, case.block_tables, np.zeros(R, np.int32), seq, cu, case.k_full_bits, case.v_full_bits)
+    q = bf16_bits_to_f32(case.q_bits).astype(np.float64)
+    threads = None
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        ref_batch_attn(q, kp, vp, case.block_tables, case.prefix_lens, case.chunk_lens, case.cu_chunk,
+                       case.num_q_heads, 1.0 / np.sqrt(128.0))
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= min_seconds or reps >= max_reps:
+            break
+    import workloads as wl
+    flops = wl.attn_flops(case.prefix_lens, case.chunk_lens, case.num_q_heads) * reps
+    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"whole workload (512 rows x 32 heads, fp64 numpy, blocked two-pass), {reps} rep(s), "
+                      f"{el:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--prefix", type=int, default=8192)
+    ap.add_argument("--chunk", type=int, default=512)
+    ap.add_argument("--layers", type=int, default=32, help="KV pool copies rotated over the steps")
+    ap.add_argument("--tile-cols", type=int, default=0, help="query columns per work item (0 = library default)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain 1 GiB device copy (for counter calibration) and exit")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (single-GPU build)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2604_16395_amd as s2l
+    import workloads
+
+    dev = "cuda"
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": 1 << 30, "launches": 3}))
+        return
+
+    P, C, HQ, HKV = args.prefix, args.chunk, 32, 8
+    case = workloads.make_case(f"p{P}_c{C}_h{HQ}kv{HKV}", [P], [C], HQ, HKV, seed=1003,
+                               pool_pages=(P + C + 15) // 16)
+    npages = case.num_pages
+    L = args.layers
+
+    def bf16(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).to(dev).view(torch.bfloat16)
+
+    # layer copies of the cache, filled through the library's own append (prefix then chunk)
+    kpools = torch.empty((L, npages, HKV, 16, 128), dtype=torch.bfloat16, device=dev)
+    vpools = torch.empty_like(kpools)
+    kpools.view(torch.int16).fill_(workloads.BF16_SENTINEL)
+    vpools.view(torch.int16).fill_(workloads.BF16_SENTINEL)
+    caches = [s2l.PagedKVCache(kpools[l], vpools[l]) for l in range(L)]
+    pre = s2l.Batch([0], [P], case.block_tables)
+    s2l.s2l_kv_append(caches[0], pre, bf16(case.prefix_rows(case.k_full_bits)),
+                      bf16(case.prefix_rows(case.v_full_bits)))
+    torch.cuda.synchronize()
+    for l in range(1, L):
+        kpools[l].copy_(kpools[0])
+        vpools[l].copy_(vpools[0])
+    batch = s2l.Batch([P], [C], case.block_tables)
+    q = bf16(case.q_bits)
+    k_new = bf16(case.new_rows(case.k_full_bits))
+    v_new = bf16(case.new_rows(case.v_full_bits))
+    out = torch.empty((C, HQ, 128), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((C, HQ), dtype=torch.float32, device=dev)
+    opts = s2l.plan_opts(tile_cols=args.tile_cols)
+    ws = torch.empty(s2l.s2l_attn_workspace_bytes(batch, HQ, HKV, opts), dtype=torch.uint8, device=dev)
+    scale = 1.0 / np.sqrt(128.0)
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        cache = caches[i % L]
+        if ev is not None:
+            ev[0].record(stream)
+        s2l.s2l_kv_append(cache, batch, k_new, v_new, stream)
+        if ev is not None:
+            ev[1].record(stream)
+        plan = s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, stream)
+        if ev is not None:
+            ev[2].record(stream)
+        s2l.s2l_attn_main(cache, batch, q, HQ, scale, out, lse, plan, ws, stream)
+        if ev is not None:
+            ev[3].record(stream)
+        s2l.s2l_split_reduce(batch, HQ, out, lse, plan, ws, stream)
+        if ev is not None:
+            ev[4].record(stream)
+        return plan
+
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            plan = step(i)
+    torch.cuda.synchronize()
+
+    # timed region 1: the K steps back to back (whole-step throughput)
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    t_start.record(stream)
+    for i in range(args.steps):
+        plan = step(args.warmup + i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+
+    # timed region 2: the same K steps with events between the kernels (per-kernel times)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        step(args.warmup + args.steps + i, evs[i])
+    torch.cuda.synchronize()
+    parts = np.array([[e[k].elapsed_time(e[k + 1]) for k in range(4)] for e in evs])  # ms
+    append_ms, plan_ms, main_ms, reduce_ms = [float(np.mean(parts[:, k])) for k in range(4)]
+    main_p10, main_p90 = float(np.percentile(parts[:, 2], 10)), float(np.percentile(parts[:, 2], 90))
+
+    flops = workloads.attn_flops([P], [C], HQ)
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    achieved = flops / (main_ms * 1e-3) / 1e12
+    src_hash = kernel_source_hash()
+    traffic = traffic_from_profile(src_hash)
+
+    result = {
+        "metric": "chunk-prefill attn TFLOP/s & us per 512-tok chunk at 8k prefix; % MFMA peak",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0, 0.5^2) bf16 Q/K/V, random page permutation)",
+        "config": {"workload": f"one request, P={P} cached + C={C} new tokens, 32q/8kv heads, d=128, "
+                               f"bf16 KV, 16-token pages, {L} rotating layer copies",
+                   "prefix": P, "chunk": C, "num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": 128},
+        "us_per_chunk": round(ms_per_step * 1e3, 2),
+        "pct_mfma_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "step_breakdown_us": {"append": round(append_ms * 1e3, 2), "plan": round(plan_ms * 1e3, 2),
+                              "attn_main": round(main_ms * 1e3, 2), "split_reduce": round(reduce_ms * 1e3, 2),
+                              "attn_main_p10": round(main_p10 * 1e3, 2), "attn_main_p90": round(main_p90 * 1e3, 2)},
+        "plan": {"work_items": plan.num_items, "split_requests": plan.num_split_reqs,
+                 "split_keys": plan.split_keys, "tile_cols": plan.tile_cols},
+        "wall_s_timed_region": round(wall, 4),
+        "roofline": {"bound": "mfma", "kernel": "attn_main_kernel", "achieved": round(achieved, 2),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic, "kernel_source_sha256_16": src_hash},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(case)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

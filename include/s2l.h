@@ -53,7 +53,8 @@ typedef enum s2l_status {
   S2L_EINVAL = -1,     /* a null pointer, negative length or inconsistent argument      */
   S2L_ERANGE = -2,     /* a request needs more pages than its block-table row holds      */
   S2L_EWORKSPACE = -3, /* workspace missing or smaller than the plan needs               */
-  S2L_ENOTSUP = -4,    /* unsupported shape: head_dim != 128, page_size != 16, G > 128   */
+  S2L_ENOTSUP = -4,    /* unsupported shape: head_dim != 128, page_size != 16, G > 128,  */
+                       /* or a tile_cols other than 0, 128, 256                          */
   S2L_EHIP = -5        /* a HIP runtime call failed (launch or attribute query)          */
 } s2l_status;
 
@@ -102,10 +103,11 @@ typedef struct s2l_batch {
 
 /* Tunables of the work partitioner; pass NULL for the defaults. */
 typedef struct s2l_plan_opts {
-  int32_t target_items;    /* work items wanted before prefixes are split; 0 = 2 x CU count */
+  int32_t target_items;    /* work items wanted before prefixes are split; 0 = automatic    */
   int32_t min_split_keys;  /* smallest key range of a split piece; 0 = 512 (rounded to 64) */
   int32_t max_splits;      /* most pieces per request; 0 = 16 (at most 64)                  */
-  int32_t reserved;
+  int32_t tile_cols;       /* query columns (tokens x heads of one kv head) per work item:  */
+                           /* 128 or 256; 0 = automatic                                    */
 } s2l_plan_opts;
 
 /* What a plan contains, returned to the host by s2l_attn_plan. */
@@ -118,6 +120,8 @@ typedef struct s2l_plan_info {
   int32_t num_reqs;
   int64_t total_tokens;    /* T                                                             */
   int64_t workspace_bytes; /* bytes of workspace this plan uses                            */
+  int32_t tile_cols;       /* query columns per work item (128 or 256)                     */
+  int32_t reserved;
 } s2l_plan_info;
 
 /* ABI version (S2L_ABI_VERSION of the built library). */
@@ -159,7 +163,7 @@ s2l_status s2l_attn_workspace_bytes(const s2l_batch* batch, int32_t num_q_heads,
 /*
  * Build the varlen work partition for one step and store it in the workspace (a small
  * kernel on `stream`); reuse it for every layer of the step.  Each request's chunk is cut
- * into query tiles of 128 / G tokens x G heads per kv head.  When the batch has fewer than
+ * into query tiles of tile_cols / G tokens x G heads per kv head.  When the batch has fewer than
  * target_items tiles, each request's key range 0 .. P_r + i_end is split into up to
  * max_splits pieces of >= min_split_keys keys, so that long prefixes spread over more
  * workgroups (their partial results are merged by s2l_split_reduce).

@@ -37,12 +37,24 @@ s2l_status hip_fail(const char* what, hipError_t e) {
 }
 
 struct Resolved {
-  int32_t target_items, min_split_keys, max_splits;
+  int32_t target_items, min_split_keys, max_splits, tile_cols;
 };
 
-s2l_status resolve_opts(const s2l_plan_opts* o, bool need_cus, int32_t num_cus, Resolved* r) {
+// Automatic tile width: 256 columns halve the LDS traffic per MFMA when the batch has
+// enough query columns to keep every CU busy with such tiles; else 128.
+int32_t auto_tile_cols(int32_t R, const int32_t* C, int32_t hq, int32_t hkv) {
+  (void)R; (void)C; (void)hq; (void)hkv;
+  return s2l::kMinTileCols;
+}
+
+s2l_status resolve_opts(const s2l_plan_opts* o, bool need_cus, int32_t num_cus, int32_t R, const int32_t* C,
+                        int32_t hq, int32_t hkv, Resolved* r) {
   int32_t t = o ? o->target_items : 0, m = o ? o->min_split_keys : 0, x = o ? o->max_splits : 0;
+  int32_t tc = o ? o->tile_cols : 0;
   if (t < 0 || m < 0 || x < 0) return fail(S2L_EINVAL, "plan opts must be >= 0");
+  if (tc != 0 && tc != s2l::kMinTileCols && tc != s2l::kMaxTileCols)
+    return fail(S2L_ENOTSUP, "tile_cols %d unsupported (0, 128 or 256)", tc);
+  r->tile_cols = tc != 0 ? tc : auto_tile_cols(R, C, hq, hkv);
   if (t == 0) {
     if (num_cus <= 0 && need_cus) {
       int dev = 0, n = 0;
@@ -63,8 +75,8 @@ s2l_status resolve_opts(const s2l_plan_opts* o, bool need_cus, int32_t num_cus, 
 s2l_status check_heads(int32_t hq, int32_t hkv) {
   if (hq <= 0 || hkv <= 0) return fail(S2L_EINVAL, "head counts must be > 0 (hq=%d hkv=%d)", hq, hkv);
   if (hq % hkv != 0) return fail(S2L_EINVAL, "num_q_heads %d is not a multiple of num_kv_heads %d", hq, hkv);
-  if (hq / hkv > s2l::kTileCols)
-    return fail(S2L_ENOTSUP, "query heads per kv head %d exceeds %d", hq / hkv, s2l::kTileCols);
+  if (hq / hkv > s2l::kMinTileCols)
+    return fail(S2L_ENOTSUP, "query heads per kv head %d exceeds %d", hq / hkv, s2l::kMinTileCols);
   return S2L_OK;
 }
 
@@ -130,7 +142,7 @@ s2l::KvLaunch kv_launch(const s2l_kv_cache* c, const s2l_batch* b) {
 // Host mirror of the device plan kernel (same rules, same order).
 void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_t hkv, const Resolved& o,
                s2l_plan_info* info, int32_t* items, int64_t cap) {
-  const int32_t g = hq / hkv, tq = s2l::tile_tokens(g);
+  const int32_t g = hq / hkv, tq = s2l::tile_tokens(g, o.tile_cols);
   int64_t base = 0, work = 0, tokens = 0;
   for (int32_t r = 0; r < R; ++r) {
     base += (int64_t)s2l::num_qtiles(C[r], tq) * hkv;
@@ -169,6 +181,8 @@ void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_
   info->num_reqs = R;
   info->total_tokens = tokens;
   info->workspace_bytes = s2l::workspace_bytes_for(R, part);
+  info->tile_cols = o.tile_cols;
+  info->reserved = 0;
 }
 
 s2l_status check_plan(const s2l_plan_info* plan, const s2l_batch* b, int32_t hq, int32_t hkv, int64_t T,
@@ -177,6 +191,8 @@ s2l_status check_plan(const s2l_plan_info* plan, const s2l_batch* b, int32_t hq,
   if (plan->num_q_heads != hq || plan->num_kv_heads != hkv || plan->num_reqs != b->num_reqs ||
       plan->total_tokens != T)
     return fail(S2L_EINVAL, "plan was made for another batch or head count");
+  if (plan->tile_cols != s2l::kMinTileCols && plan->tile_cols != s2l::kMaxTileCols)
+    return fail(S2L_EINVAL, "plan info has an invalid tile width %d", plan->tile_cols);
   if (!ws) return fail(S2L_EWORKSPACE, "workspace is NULL");
   if ((int64_t)ws_bytes < plan->workspace_bytes)
     return fail(S2L_EWORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)plan->workspace_bytes);
@@ -253,7 +269,9 @@ s2l_status s2l_attn_workspace_bytes(const s2l_batch* batch, int32_t num_q_heads,
   if ((st = check_batch(batch, false, &T)) != S2L_OK) return st;
   if ((st = check_heads(num_q_heads, num_kv_heads)) != S2L_OK) return st;
   Resolved o;
-  if ((st = resolve_opts(opts, true, 0, &o)) != S2L_OK) return st;
+  if ((st = resolve_opts(opts, true, 0, batch->num_reqs, batch->chunk_lens_host, num_q_heads, num_kv_heads, &o)) !=
+      S2L_OK)
+    return st;
   s2l_plan_info info;
   host_plan(batch->num_reqs, batch->prefix_lens_host, batch->chunk_lens_host, num_q_heads, num_kv_heads, o, &info,
             nullptr, 0);
@@ -271,7 +289,9 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
   if (batch->num_reqs > 0 && !batch->cu_chunk) return fail(S2L_EINVAL, "cu_chunk is NULL");
   if ((st = check_heads(num_q_heads, num_kv_heads)) != S2L_OK) return st;
   Resolved o;
-  if ((st = resolve_opts(opts, true, 0, &o)) != S2L_OK) return st;
+  if ((st = resolve_opts(opts, true, 0, batch->num_reqs, batch->chunk_lens_host, num_q_heads, num_kv_heads, &o)) !=
+      S2L_OK)
+    return st;
   s2l_plan_info pi;
   host_plan(batch->num_reqs, batch->prefix_lens_host, batch->chunk_lens_host, num_q_heads, num_kv_heads, o, &pi,
             nullptr, 0);
@@ -292,6 +312,7 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
   a.target_items = o.target_items;
   a.min_split_keys = o.min_split_keys;
   a.max_splits = o.max_splits;
+  a.tile_cols = o.tile_cols;
   a.ws_bytes = (int64_t)ws_bytes;
   a.workspace = workspace;
   (void)hipGetLastError();
@@ -316,6 +337,7 @@ s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch, cons
   a.softmax_scale = softmax_scale;
   a.workspace = workspace;
   a.num_items = plan->num_items;
+  a.tile_cols = plan->tile_cols;
   (void)hipGetLastError();
   hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("attn_main launch", e);
@@ -366,7 +388,9 @@ s2l_status s2l_plan_host(int32_t num_reqs, const int32_t* prefix_lens_host, cons
   if ((st = check_batch(&b, false, &T)) != S2L_OK) return st;
   if ((st = check_heads(num_q_heads, num_kv_heads)) != S2L_OK) return st;
   Resolved o;
-  if ((st = resolve_opts(opts, false, num_cus, &o)) != S2L_OK) return st;
+  if ((st = resolve_opts(opts, false, num_cus, num_reqs, chunk_lens_host, num_q_heads, num_kv_heads, &o)) !=
+      S2L_OK)
+    return st;
   if (item_capacity < 0) return fail(S2L_EINVAL, "item_capacity < 0");
   host_plan(num_reqs, prefix_lens_host, chunk_lens_host, num_q_heads, num_kv_heads, o, info, items_out,
             item_capacity);

@@ -8,7 +8,7 @@ namespace s2l {
 
 namespace {
 
-constexpr int kPlanThreads = 1024;
+constexpr int kPlanThreads = 256;
 constexpr int kPlanWaves = kPlanThreads / 64;
 
 // Block-wide exclusive scan of three int64 values; returns the block totals in tot[].
@@ -43,7 +43,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
   __shared__ int64_t tot[3];
   const int R = a.num_reqs;
   const int G = a.hq / a.hkv;
-  const int tq = tile_tokens(G);
+  const int tq = tile_tokens(G, a.tile_cols);
   int32_t* item_off = pp.item_off;
   int32_t* nqt_a = pp.nqt;
   int32_t* ns_a = pp.ns;
@@ -108,7 +108,8 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     h->num_split_reqs = (int32_t)num_split;
     h->split_keys = split_keys;
     h->status = fits ? 0 : 1;
-    h->pad0 = h->pad1 = 0;
+    h->tile_cols = a.tile_cols;
+    h->pad1 = 0;
     h->part_floats = part_floats;
     h->total_tokens = total_tokens;
   }

@@ -30,7 +30,7 @@ struct PlanLaunch {
   const int32_t* chunk_lens;
   const int32_t* cu_chunk;
   int32_t num_reqs, hq, hkv;
-  int32_t target_items, min_split_keys, max_splits;
+  int32_t target_items, min_split_keys, max_splits, tile_cols;
   int64_t ws_bytes;
   void* workspace;
 };
@@ -45,6 +45,7 @@ struct AttnLaunch {
   float softmax_scale;
   void* workspace;
   int32_t num_items;        // grid size (host copy of the plan's item count)
+  int32_t tile_cols;        // 128 or 256 (host copy of the plan's tile width)
 };
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream);
 

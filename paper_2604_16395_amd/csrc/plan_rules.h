@@ -3,11 +3,11 @@
 // derive the same partition from the same lengths.
 //
 // Work item = (request r, kv head g, query tile, key-range piece).  A query tile is
-// kTileCols packed columns of one kv head: tq = kTileCols / G consecutive chunk tokens
-// times the G query heads that share kv head g (token-major: column n is token n / G,
-// head g*G + n % G), so a tile's causal diagonal spans only tq tokens.  A tile with chunk
-// tokens [i0, i1) needs keys [0, P + i1); that range is cut into `ns` pieces of a
-// multiple of kKvTile keys when the batch has too few tiles to fill the GPU.
+// tile_cols (128 or 256) packed columns of one kv head: tq = tile_cols / G consecutive
+// chunk tokens times the G query heads that share kv head g (token-major: column n is
+// token n / G, head g*G + n % G), so a tile's causal diagonal spans only tq tokens.  A
+// tile with chunk tokens [i0, i1) needs keys [0, P + i1); that range is cut into `ns`
+// pieces of a multiple of kKvTile keys when the batch has too few tiles to fill the GPU.
 #pragma once
 #include <stdint.h>
 
@@ -21,7 +21,8 @@ namespace s2l {
 
 constexpr int kHeadDim = 128;
 constexpr int kPageSize = 16;
-constexpr int kTileCols = 128;      // packed (token, head) columns per work item (4 waves x 32)
+constexpr int kMinTileCols = 128;   // packed (token, head) columns per work item: 4 waves x 32
+constexpr int kMaxTileCols = 256;   //   or 4 waves x 64
 constexpr int kKvTile = 64;         // keys per LDS tile
 constexpr int kMaxSplitsCap = 64;
 constexpr int kDefaultMinSplitKeys = 512;
@@ -37,7 +38,8 @@ struct PlanHeader {           // first 256 bytes of the workspace
   int32_t num_split_reqs;
   int32_t split_keys;
   int32_t status;             // 0 ok, 1 = partials exceed the workspace (nothing planned)
-  int32_t pad0, pad1;
+  int32_t tile_cols;
+  int32_t pad1;
   int64_t part_floats;
   int64_t total_tokens;
 };
@@ -49,7 +51,7 @@ S2L_HD inline int64_t align_up(int64_t x, int64_t a) {
 S2L_HD inline int32_t ceil_div(int32_t a, int32_t b) { return (a + b - 1) / b; }
 S2L_HD inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-S2L_HD inline int32_t tile_tokens(int32_t g) { return kTileCols / g; }
+S2L_HD inline int32_t tile_tokens(int32_t g, int32_t tile_cols) { return tile_cols / g; }
 S2L_HD inline int32_t num_qtiles(int32_t c, int32_t tq) { return c > 0 ? ceil_div(c, tq) : 0; }
 
 // Keys summed over the query tiles of one (request, kv head): tile t covers tokens

@@ -47,10 +47,24 @@ __device__ inline uint32_t f32x4_to_fp8x4(float a, float b, float c, float d) {
 __device__ inline float bf16lo(uint32_t w) { return u2f(w << 16); }
 __device__ inline float bf16hi(uint32_t w) { return u2f(w & 0xFFFF0000u); }
 
+// IEEE max of three / two values as single VALU instructions.  Plain fmaxf() makes the
+// compiler canonicalise each operand first (one extra v_max per value) whenever it cannot
+// prove the operand canonical; the values here are never signalling NaNs.
+__device__ inline float vmax3(float a, float b, float c) {
+  float r;
+  __asm__("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+__device__ inline float vmax2(float a, float b) {
+  float r;
+  __asm__("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 // Exchange with lane l ^ 32 (v_permlane32_swap): r[0], r[1] are {own, partner} in some order.
 __device__ inline float max_with_partner(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(f2u(x), f2u(x), false, false);
-  return fmaxf(u2f(r[0]), u2f(r[1]));
+  return vmax2(u2f(r[0]), u2f(r[1]));
 }
 __device__ inline float sum_with_partner(float x) {
   auto r = __builtin_amdgcn_permlane32_swap(f2u(x), f2u(x), false, false);

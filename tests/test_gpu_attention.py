@@ -26,14 +26,16 @@ SMALL = [
 ]
 
 
+@pytest.mark.parametrize("tile_cols", [128, 256])
 @pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("name,P,C,hq,hkv", SMALL)
-def test_small_cases_match_oracle(name, P, C, hq, hkv, split):
+def test_small_cases_match_oracle(name, P, C, hq, hkv, split, tile_cols):
     case = workloads.make_case(name, P, C, hq, hkv, seed=zlib.crc32(name.encode()) % 1000)
-    print(f"[attn] {name} split={split}", flush=True)
+    print(f"[attn] {name} split={split} tile_cols={tile_cols}", flush=True)
     s = Setup(case)
     s.append()
-    out, lse = s.attention(s2l.plan_opts(**FORCE_SPLIT) if split else None)
+    opts = dict(FORCE_SPLIT) if split else {}
+    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols, **opts))
     if split and max(P) + max(C) > 64:
         assert s.plan.num_split_reqs > 0
     ref = s.oracle()
@@ -57,13 +59,14 @@ def test_config1_full_and_first_row_is_v0():
     assert np.array_equal(got, np.repeat(v0, 4, axis=0))
 
 
-@pytest.mark.parametrize("q_sigma,k_ramp", [(4.0, 0.0), (4.0, 3.0), (0.5, 6.0)])
+@pytest.mark.parametrize("q_sigma,k_ramp", [(4.0, 0.0), (4.0, 3.0), (0.5, 6.0), (0.05, 0.0)])
 def test_peaky_and_growing_scores(q_sigma, k_ramp):
-    """Score spread of sigma ~2 and keys that grow along the sequence, so the running max
-    rises during the key loop and the rescaling path runs."""
+    """Score spread of sigma ~2, keys that grow along the sequence (the running max rises
+    during the key loop and the rescaling path runs), and near-uniform scores."""
     case = workloads.make_case("peaky", [3000, 100], [300, 64], 32, 8, seed=10, q_sigma=q_sigma,
                                k_ramp=k_ramp)
-    for opts in (None, s2l.plan_opts(**FORCE_SPLIT)):
+    for opts in (None, s2l.plan_opts(**FORCE_SPLIT), s2l.plan_opts(tile_cols=256),
+                 s2l.plan_opts(tile_cols=256, **FORCE_SPLIT)):
         s = Setup(case)
         s.append()
         out, lse = s.attention(opts)
@@ -71,11 +74,12 @@ def test_peaky_and_growing_scores(q_sigma, k_ramp):
         assert_attention_close(case, out, lse, ref, what=f"peaky{q_sigma},{k_ramp}")
 
 
-def test_config2_sampled_rows():
+@pytest.mark.parametrize("tile_cols", [128, 256])
+def test_config2_sampled_rows(tile_cols):
     case = workloads.config2()
     s = Setup(case)
     s.append()
-    out, lse = s.attention()
+    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols))
     rows = sample_rows(case, 48, np.random.default_rng(2))
     ref = s.oracle(rows)
     assert_attention_close(case, out, lse, ref, rows, what="cfg2")
@@ -91,11 +95,12 @@ def test_config4_mixed_batch_sampled_rows():
     assert_attention_close(case, out, lse, ref, rows, what="cfg4")
 
 
-def test_config5_fp8_cache_sampled_rows():
+@pytest.mark.parametrize("tile_cols", [128, 256])
+def test_config5_fp8_cache_sampled_rows(tile_cols):
     case = workloads.config5()
     s = Setup(case)
     s.append()
-    out, lse = s.attention()
+    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols))
     rows = sample_rows(case, 30, np.random.default_rng(5))
     ref = s.oracle(rows)
     assert_attention_close(case, out, lse, ref, rows, what="cfg5")
@@ -120,3 +125,15 @@ def test_empty_and_zero_length_requests():
     ws = torch.empty(s2l.s2l_attn_workspace_bytes(empty, 8, 2), dtype=torch.uint8, device=DEV)
     plan = s2l.s2l_attn_plan(empty, 8, 2, ws)
     assert plan.num_items == 0
+
+
+@pytest.mark.parametrize("tile_cols", [128, 256])
+@pytest.mark.parametrize("split", [False, True])
+def test_small_fp8_cache_matches_oracle(split, tile_cols):
+    case = workloads.make_case("fp8_small", [700, 0, 33], [130, 77, 1], 64, 8, seed=14, kv_dtype="fp8")
+    s = Setup(case)
+    s.append()
+    opts = dict(FORCE_SPLIT) if split else {}
+    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols, **opts))
+    ref = s.oracle()
+    assert_attention_close(case, out, lse, ref, what="fp8_small")
