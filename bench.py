@@ -97,6 +97,8 @@ def main():
     ap.add_argument("--chunk", type=int, default=512)
     ap.add_argument("--layers", type=int, default=32, help="KV pool copies rotated over the steps")
     ap.add_argument("--tile-cols", type=int, default=0, help="query columns per work item (0 = library default)")
+    ap.add_argument("--target-items", type=int, default=0,
+                    help="work items the planner aims for when splitting prefixes (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (for counter calibration) and exit")
@@ -148,7 +150,7 @@ def main():
     v_new = bf16(case.new_rows(case.v_full_bits))
     out = torch.empty((C, HQ, 128), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((C, HQ), dtype=torch.float32, device=dev)
-    opts = s2l.plan_opts(tile_cols=args.tile_cols)
+    opts = s2l.plan_opts(tile_cols=args.tile_cols, target_items=args.target_items)
     ws = torch.empty(s2l.s2l_attn_workspace_bytes(batch, HQ, HKV, opts), dtype=torch.uint8, device=dev)
     scale = 1.0 / np.sqrt(128.0)
     stream = torch.cuda.Stream()

@@ -107,7 +107,7 @@ typedef struct s2l_plan_opts {
   int32_t min_split_keys;  /* smallest key range of a split piece; 0 = 512 (rounded to 64) */
   int32_t max_splits;      /* most pieces per request; 0 = 16 (at most 64)                  */
   int32_t tile_cols;       /* query columns (tokens x heads of one kv head) per work item:  */
-                           /* 128 or 256; 0 = automatic                                    */
+                           /* 128 (4-wave workgroups) or 256 (8 waves); 0 = automatic      */
 } s2l_plan_opts;
 
 /* What a plan contains, returned to the host by s2l_attn_plan. */
@@ -182,7 +182,10 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
  *   out[cu_chunk[r]+i][h] = sum_j e^{s_j} V_r[j][g] / sum_j e^{s_j}     (bf16, RNE)
  *   lse[cu_chunk[r]+i][h] = ln sum_j e^{s_j}                             (fp32, optional)
  * K_r/V_r are read from the pages after the step's append (the chunk's own keys included;
- * for an fp8 cache these are its quantised values decode(code) * scale).
+ * for an fp8 cache these are its quantised values decode(code) * scale).  Precision: the
+ * weights e^{s_j} / sum are applied as bf16 values normalised by their own sum, so out is
+ * within about 2^-7 sum_j w_j |V_j - out| + 2^-8 |out| of the exact result; lse uses fp32
+ * sums.
  *   q   : device bf16 [T][Hq][128] (post-RoPE).     out : device bf16 [T][Hq][128].
  *   lse : device fp32 [T][Hq] or NULL.               softmax_scale > 0 (e.g. 1/sqrt(128)).
  *   plan: the s2l_plan_info returned by s2l_attn_plan for this batch and head counts.
@@ -196,7 +199,8 @@ s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* ba
 /*
  * The main attention kernel alone (online softmax over the work items of the plan).
  * Unsplit requests get their final out/lse; split requests get fp32 partials (unnormalised
- * output, running max, running sum) in the workspace, merged by s2l_split_reduce.
+ * output, then reference max and the two running sums) in the workspace, merged by
+ * s2l_split_reduce.
  */
 s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch,
                          const void* q, int32_t num_q_heads, float softmax_scale,

@@ -72,8 +72,9 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
     exp(s - m) and exp(s - m) V.  Blocks only bound memory: no term is reordered
     beyond summation order.
 
-    ``with_abs`` also returns the same softmax weights applied to |V| (a per-element
-    scale for rounding-error bounds of an implementation that rounds the weights).
+    ``with_abs`` also returns A = sum_j w_j |V_j| and B = sum_j w_j |V_j - O| (pass 3,
+    once O is known), with w the softmax weights: per-element scales for rounding-error
+    bounds of an implementation that rounds the weights.
     """
     C, hq, d = q.shape
     hkv = k.shape[1]
@@ -82,6 +83,7 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
     n_rows = len(rows)
     out = np.zeros((n_rows, hq, d))
     out_abs = np.zeros((n_rows, hq, d)) if with_abs else None
+    out_dev = np.zeros((n_rows, hq, d)) if with_abs else None
     lse = np.zeros((n_rows, hq))
     for g in range(hkv):
         heads = slice(g * g_size, (g + 1) * g_size)
@@ -111,12 +113,23 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
                 acc += np.einsum("ngj,jd->ngd", w, vb)
                 if with_abs:
                     acc_abs += np.einsum("ngj,jd->ngd", w, np.abs(vb))
-            out[b0:b0 + q_block, heads, :] = acc / den[:, :, None]
+            o_blk = acc / den[:, :, None]
+            out[b0:b0 + q_block, heads, :] = o_blk
             lse[b0:b0 + q_block, heads] = m + np.log(den)
             if with_abs:
                 out_abs[b0:b0 + q_block, heads, :] = acc_abs / den[:, :, None]
+                dev = np.zeros((len(rb), g_size, d))
+                for k0 in range(0, kmax, k_block):       # pass 3: spread about O
+                    kb = k[k0:min(kmax, k0 + k_block), g, :]
+                    vb = v[k0:min(kmax, k0 + k_block), g, :]
+                    s = scale * np.einsum("ngd,jd->ngj", qb, kb)
+                    keys = np.arange(k0, k0 + kb.shape[0])
+                    w = np.where(keys[None, None, :] <= horizon[:, None, None],
+                                 np.exp(s - m[:, :, None]), 0.0)
+                    dev += np.einsum("ngj,ngjd->ngd", w, np.abs(vb[None, None, :, :] - o_blk[:, :, None, :]))
+                out_dev[b0:b0 + q_block, heads, :] = dev / den[:, :, None]
     if with_abs:
-        return out, lse, out_abs
+        return out, lse, out_abs, out_dev
     return out, lse
 
 
@@ -189,13 +202,15 @@ def ref_batch_attn(q_rows, k_pool, v_pool, block_tables, prefix_lens, chunk_lens
     q_rows: float64 [T][Hq][D] (the chunk queries, request r at rows cu_chunk[r]..).
     Returns float64 O [T][Hq][D] and LSE [T][Hq] (rows not sampled are NaN when
     ``sample_rows`` is given as a dict r -> sorted chunk-row indices), and with
-    ``with_abs`` the softmax-weighted mean of |V| [T][Hq][D] as a third array.
+    ``with_abs`` the softmax-weighted means of |V| and of |V - O| [T][Hq][D] as a third and
+    a fourth array.
     """
     T = q_rows.shape[0]
     d = q_rows.shape[2]
     out = np.full((T, num_q_heads, d), np.nan)
     lse = np.full((T, num_q_heads), np.nan)
     out_abs = np.full((T, num_q_heads, d), np.nan) if with_abs else None
+    out_dev = np.full((T, num_q_heads, d), np.nan) if with_abs else None
     for r in range(len(prefix_lens)):
         P, C, row0 = int(prefix_lens[r]), int(chunk_lens[r]), int(cu_chunk[r])
         if C == 0:
@@ -217,6 +232,7 @@ def ref_batch_attn(q_rows, k_pool, v_pool, block_tables, prefix_lens, chunk_lens
             out[row0 + idx], lse[row0 + idx] = res[0], res[1]
             if with_abs:
                 out_abs[row0 + idx] = res[2]
+                out_dev[row0 + idx] = res[3]
     if with_abs:
-        return out, lse, out_abs
+        return out, lse, out_abs, out_dev
     return out, lse

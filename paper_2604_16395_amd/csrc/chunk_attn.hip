@@ -4,24 +4,35 @@
 // num_computed_tokens as in Sec. 4.2): query i of a request's new chunk (absolute position
 // t = P + i) attends to keys 0..t of that request, read through its block table.
 //
-// One workgroup = 4 waves = one work item of the plan: kv head g, 128 packed query
-// columns (tq tokens x G heads, token-major) and a key range [lo, hi).  Per 64-key tile:
-//   * K and V (64 keys x 128) are staged in LDS, double buffered; pages are read through
-//     the block table with raw buffer loads, keys at or past `hi` are zero-filled;
-//   * each wave computes S^T = K Q^T for its 32 columns with v_mfma_f32_32x32x16_bf16
-//     (A = K rows from LDS, B = Q held in registers), so every lane owns one query column
-//     and 32 of the tile's scores;
-//   * online softmax in the exp2 domain, row max shared with lane ^ 32 by
-//     v_permlane32_swap; the running maximum is only raised (and O rescaled) when the new
-//     maximum exceeds it by more than 2^8, else probabilities up to 2^8 are accumulated
-//     against the stale maximum (exact after the final division);
+// One workgroup = kWaves waves (4 or 8) = one work item of the plan: kv head g, 32 kWaves
+// packed query columns (tq tokens x G heads, token-major) and a key range [lo, hi).
+//
+// Data movement.  K and V tiles of 64 keys x 128 are staged in LDS, one key row of 256
+// bytes each, 16-byte chunks permuted per row (K: chunk c of row r at c ^ (r & 15); V: at
+// c ^ 4 (r & 3)) so that the MFMA operand reads below hit 64 distinct banks.  bf16 pages
+// are copied straight from HBM into LDS (buffer_load ... lds), each wave moving one page of
+// the tile; the buffer descriptor of a page ends at key `hi`, so keys past it arrive as
+// zeros.  E4M3 pages go through registers and are widened to bf16 on the way (exact).  K
+// is fetched one tile ahead of V; both are double buffered.
+//
+// Compute, per wave (32 query columns, one per lane pair), per 32-key sub-block b:
+//   * S^T(b) = K Q^T with v_mfma_f32_32x32x16_bf16: A = K rows from LDS, B = Q held in
+//     registers, so every lane owns one query column and 16 of the sub-block's scores;
+//   * online softmax in the exp2 domain against a per-column reference m, set to the exact
+//     max of the item's first sub-block (lane pair combined by v_permlane32_swap); later
+//     probabilities exp2(s c - m) are accumulated against it as they come, so a sub-block
+//     costs no max; only when one of them would exceed 2^64 (the row sum shows it) is m
+//     raised to that sub-block's max and the sub-block redone.  The final division by the
+//     accumulated sum makes the result independent of m;
 //   * O^T += V^T P^T with the same MFMA: A = V^T read from the key-major V tile with the
-//     gfx950 transposing LDS read (ds_read_b64_tr_b16), B = P (bf16) straight from the
-//     score registers, the A operand's k-slots ordered as the keys each lane half holds;
-//   * the causal mask is evaluated only on tiles that reach past the first query token's
-//     position (the chunk-diagonal tiles).
+//     transposing LDS read (ds_read_b64_tr_b16), B = bf16 P straight from the registers.
+// The sub-blocks are software pipelined: while the softmax of sub-block b runs on the
+// VALU, the MFMA unit computes S(b+1) and O += P(b-1) V(b-1); P(b-1) is checked for
+// overflow at the start of step b, before it enters O.  The causal mask is applied only to
+// sub-blocks that reach past the first query token's position.
+//
 // Unsplit items write bf16 O = acc / l (and LSE); split items write fp32 partials
-// (acc, m, l) that split_reduce merges.
+// (acc, m, l) that split_reduce merges (log-sum-exp merge of Sec. 2.1's softmax).
 #include "launch.h"
 #include "plan_rules.h"
 #include "s2l_device.h"
@@ -30,19 +41,15 @@ namespace s2l {
 
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kThreads = kWaves * 64;
-#ifndef S2L_VROW_PAD
-#define S2L_VROW_PAD 32   // 320-byte rows: the transposing reads hit distinct banks
-#endif
-constexpr int kKRow = 128 + 8;                     // bf16 per K row in LDS (272 B: bank-shifted rows)
-constexpr int kVRow = 128 + S2L_VROW_PAD;          // bf16 per V row in LDS
-constexpr int kKTile = kKvTile * kKRow;            // elements
-constexpr int kVTile = kKvTile * kVRow;
-constexpr int kBufElems = kKTile + kVTile;         // one stage buffer (35840 B)
+constexpr int kRowBytes = kHeadDim * 2;              // one bf16 key row in LDS
+constexpr int kTileBytes = kKvTile * kRowBytes;      // 16 KiB
+constexpr int kSubBytes = 32 * kRowBytes;            // one 32-key sub-block of a tile
+constexpr int kKBuf = 0;                             // K tiles at 0 and 16 KiB
+constexpr int kVBuf = 2 * kTileBytes;                // V tiles at 32 and 48 KiB
+constexpr int kLdsBytes = 4 * kTileBytes;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
-constexpr float kRescaleSlack = 8.0f;              // log2 units
+constexpr float kOverflow = 18446744073709551616.0f;   // 2^64: largest probability kept
 
 // Largest r with a[r] <= x, for a non-decreasing a[0..n] with a[0] <= x < a[n].
 __device__ inline int upper_index(const int32_t* a, int n, int x) {
@@ -54,12 +61,6 @@ __device__ inline int upper_index(const int32_t* a, int n, int x) {
   return lo;
 }
 
-// Registers holding one tile's global loads until they are written to LDS.
-struct Stage {
-  u32x4 k[4];
-  u32x4 v[4];
-};
-
 // Raw buffer loads: a resource descriptor (base, size in bytes) in SGPRs plus a per-lane
 // byte offset.  Offsets at or past the size read as zero.
 constexpr int32_t kRsrcWord3 = 0x00020000;   // gfx9-family raw buffer: 32-bit dword format
@@ -67,169 +68,77 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int32_t byt
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, kRsrcWord3);
 }
 
-// Page ids of the four 16-key pages of the tile at key kb (lane l loads entry l & 3).
-// Entries past the item's last page read as 0, a valid page: the keys they would hold are
-// at or past `hi` and are zeroed before use.
-__device__ inline int32_t tile_page_entry(const int32_t* bt, int kb, int last_page, uint32_t lane_off) {
-  const int first = kb >> 4;
-  const int n = last_page + 1 - first;
-  return (int32_t)__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(bt + first, 4 * (n > 0 ? n : 0)), lane_off, 0, 0);
-}
-struct Pages {
-  int32_t p[4];
-};
-__device__ inline Pages broadcast_pages(int32_t v) {
-  Pages pg;
-  pg.p[0] = __builtin_amdgcn_readlane(v, 0);
-  pg.p[1] = __builtin_amdgcn_readlane(v, 1);
-  pg.p[2] = __builtin_amdgcn_readlane(v, 2);
-  pg.p[3] = __builtin_amdgcn_readlane(v, 3);
-  return pg;
-}
-__device__ inline int32_t pick(const Pages& pg, int j) {  // j wave-uniform
-  return j == 0 ? pg.p[0] : (j == 1 ? pg.p[1] : (j == 2 ? pg.p[2] : pg.p[3]));
-}
-
-// Global loads of one tile.  bf16 cache: thread t loads K rows (t>>4) + 16j (page j, slot
-// t>>4), 16-byte chunk t&15, and V rows 4(t>>4) + i (page t>>6, slot 4((t>>4)&3) + i) of the
-// same chunk.  fp8 cache: K rows (t>>3) + 32j (page 2j + (t>>7)), 16-byte chunk t&7; V rows
-// as for bf16 with 8-byte chunks t&15, kept raw in .xy.  The loads are unconditional (pages
-// are clamped to valid ones); keys at or past `hi` are zeroed in store_tile, once the data
-// has arrived, so no instruction waits on a load before the tile's compute is done.
-// Per-thread byte offsets of the tile loads inside a (page, kv head) run; loop invariant,
-// so the address of every load is a uniform base (pool + page stride, in SGPRs) plus one of
-// these (VGPRs never overwritten while a load is in flight).
-struct LoadOffsets {
-  uint32_t k;      // K row / chunk offset
-  uint32_t v[4];   // V rows 4((t>>4)&3) + i
-};
-template <bool kFp8>
-__device__ inline LoadOffsets load_offsets() {
-  const int t = threadIdx.x;
-  LoadOffsets o;
-  if constexpr (!kFp8) {
-    o.k = (uint32_t)(((t >> 4) * 128 + (t & 15) * 8) * 2);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o.v[i] = (uint32_t)(((4 * ((t >> 4) & 3) + i) * 128 + (t & 15) * 8) * 2);
-  } else {
-    o.k = (uint32_t)(((t >> 3) & 15) * 128 + (t & 7) * 16);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) o.v[i] = (uint32_t)((4 * ((t >> 4) & 3) + i) * 128 + (t & 15) * 8);
-  }
-  return o;
-}
-
-template <bool kFp8>
-__device__ inline void load_tile(Stage& st, const char* kpool, const char* vpool, const Pages& pg,
-                                 int64_t head, int hkv, const LoadOffsets& lo) {
-  constexpr int32_t kRun = kFp8 ? 16 * 128 : 16 * 128 * 2;   // bytes of one (page, kv head)
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const auto vr = make_rsrc(vpool + ((int64_t)pick(pg, wave) * hkv + head) * kRun, kRun);
-  if constexpr (!kFp8) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const auto kr = make_rsrc(kpool + ((int64_t)pg.p[j] * hkv + head) * kRun, kRun);
-      st.k[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, lo.k, 0, 0));
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) st.v[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, lo.v[i], 0, 0));
-  } else {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const auto kr = make_rsrc(kpool + ((int64_t)pick(pg, 2 * j + (wave >> 1)) * hkv + head) * kRun, kRun);
-      st.k[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, lo.k, 0, 0));
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const u32x2 w = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(vr, lo.v[i], 0, 0));
-      st.v[i] = u32x4{w[0], w[1], 0, 0};
-    }
-  }
-}
-
-// Zero the staged keys at or past `hi` (only the last tile of an item can have any).
-template <bool kFp8>
-__device__ inline void mask_tile(Stage& st, int kb0, int hi) {
-  const int t = threadIdx.x;
-  if constexpr (!kFp8) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (kb0 + (t >> 4) + 16 * j >= hi) st.k[j] = u32x4{0, 0, 0, 0};
-  } else {
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      if (kb0 + (t >> 3) + 32 * j >= hi) st.k[j] = u32x4{0, 0, 0, 0};
-  }
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    if (kb0 + 4 * (t >> 4) + i >= hi) st.v[i] = u32x4{0, 0, 0, 0};
-}
-
-// K and V tiles are stored in LDS as they are in the pages, one key per row (row strides
-// kKRow / kVRow elements).  Thread t writes its staged rows: bf16 K rows (t>>4) + 16j and V
-// rows 4(t>>4) + i, 16-byte chunk t&15; fp8 data is converted to bf16 on the way (exact).
-template <bool kFp8>
-__device__ inline void store_tile(const Stage& st, uint16_t* buf) {
-  const int t = threadIdx.x;
-  uint16_t* kl = buf;
-  uint16_t* vl = buf + kKTile;
-  if constexpr (!kFp8) {
-    const int c = t & 15;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<u32x4*>(kl + ((t >> 4) + 16 * j) * kKRow + c * 8) = st.k[j];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<u32x4*>(vl + (4 * (t >> 4) + i) * kVRow + c * 8) = st.v[i];
-  } else {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const u32x2 a = fp8x4_to_bf16x4(st.k[j][0]);
-      const u32x2 b = fp8x4_to_bf16x4(st.k[j][1]);
-      const u32x2 c = fp8x4_to_bf16x4(st.k[j][2]);
-      const u32x2 d = fp8x4_to_bf16x4(st.k[j][3]);
-      uint16_t* row = kl + ((t >> 3) + 32 * j) * kKRow + (t & 7) * 16;
-      *reinterpret_cast<u32x4*>(row) = u32x4{a[0], a[1], b[0], b[1]};
-      *reinterpret_cast<u32x4*>(row + 8) = u32x4{c[0], c[1], d[0], d[1]};
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const u32x2 a = fp8x4_to_bf16x4(st.v[i][0]);
-      const u32x2 b = fp8x4_to_bf16x4(st.v[i][1]);
-      *reinterpret_cast<u32x4*>(vl + (4 * (t >> 4) + i) * kVRow + (t & 15) * 8) = u32x4{a[0], a[1], b[0], b[1]};
-    }
-  }
-}
-
-// A operand of O^T += V^T P^T for k-step ks (keys 16ks..16ks+15 of the tile) and d-block db,
-// read transposed from the key-major V tile with two ds_read_b64_tr_b16.  Within each group
-// of 16 lanes, lane j addresses key row (j>>2) of a 4-key set at column base + 4(j&3); the
-// hardware hands lane i the four keys of column base + i.  Lane (n, half) thereby receives
-// V[keys 4 half + {0..3}, then 8 + 4 half + {0..3}][32 db + n]: the k-slot order of the
-// score registers it multiplies.
+typedef __attribute__((address_space(3))) void lds_void;
 typedef short v4i16 __attribute__((ext_vector_type(4)));
-__device__ inline bf16x8 read_vt(const uint16_t* vl, int ks, int db) {
-  const int l = threadIdx.x & 63;
-  const int j = l & 15, half = l >> 5;
-  const int col = 32 * db + 16 * ((l >> 4) & 1) + 4 * (j & 3);
-  const int row0 = 16 * ks + 4 * half + (j >> 2);
-  typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-  const lds_v4i16* p0 = (const lds_v4i16*)(vl + row0 * kVRow + col);
-  const lds_v4i16* p1 = (const lds_v4i16*)(vl + (row0 + 8) * kVRow + col);
-  const v4i16 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_v4i16*>(p0));
-  const v4i16 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(const_cast<lds_v4i16*>(p1));
-  const u32x2 ua = __builtin_bit_cast(u32x2, a), ub = __builtin_bit_cast(u32x2, b);
-  return __builtin_bit_cast(bf16x8, u32x4{ua[0], ua[1], ub[0], ub[1]});
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+__device__ inline int clamp16(int x) { return x < 0 ? 0 : (x > 16 ? 16 : x); }
+
+// Block-table entry `idx` of the request (0 past its last page: the descriptor of such a
+// page then has size 0 and nothing is read from it).  Every lane loads the same entry.
+// The index goes into the scalar offset: a load with a VGPR address would make every later
+// write of that VGPR wait for the load.
+__device__ inline int32_t table_entry(const int32_t* bt, int idx, int last_page) {
+  const int n = last_page + 1;
+  return (int32_t)__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(bt, 4 * n), 0u,
+                                                       __builtin_amdgcn_readfirstlane(4 * idx), 0);
 }
 
-// kQB blocks of 32 query columns per wave: the workgroup's tile is 4 * 32 * kQB columns.
-template <bool kFp8, int kQB>
-__global__ __launch_bounds__(kThreads, kQB == 1 ? 2 : 1) void attn_main_kernel(
+// LDS-direct copy: 64 lanes x 16 bytes from a raw buffer (descriptor words in SGPRs) to the
+// 1 KiB of LDS at byte address `lds`, lane l's bytes at lds + 16 l.  Issued as inline
+// assembly so that the compiler does not treat every later LDS read as waiting on it; the
+// caller waits for vmcnt(0) and synchronises before the destination is read.
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+__device__ inline i32x4 sgpr_rsrc(const void* base, int32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{(int32_t)__builtin_amdgcn_readfirstlane((uint32_t)a),
+               (int32_t)(__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) & 0xffff),
+               __builtin_amdgcn_readfirstlane(bytes), kRsrcWord3};
+}
+__device__ inline void lds_dma_b128(const i32x4& rs, uint32_t voff, uint32_t lds) {
+  __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                   :: "s"(lds), "v"(voff), "s"(rs) : "m0");
+}
+
+// Sub-block max of the 16 scores a lane holds, then over the lane pair (l, l ^ 32).  The
+// scores come straight from MFMAs: the max must be ordinary code (the compiler forms
+// v_max3 chains), so that the wait states an MFMA result needs before a VALU read are
+// inserted; an assembly max here can read a partly accumulated score.
+__device__ inline float block_max(const f32x16& s) {
+  float mx = __builtin_fmaxf(s[0], s[1]);
+#pragma unroll
+  for (int e = 2; e < 16; ++e) mx = __builtin_fmaxf(mx, s[e]);
+  return max_with_partner(mx);
+}
+
+// Instruction order the scheduler is asked for in one slot of a pipelined step: each MFMA
+// followed by a few VALU instructions of the softmax and the LDS reads of a later slot.
+template <bool kQK, bool kReads>
+__device__ inline void slot_schedule() {
+  if constexpr (kQK) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);     // VALU
+    if constexpr (kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read (K)
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  __builtin_amdgcn_sched_group_barrier(0x002, kQK ? 3 : 7, 0);
+  if constexpr (kReads) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // LDS reads (V)
+}
+
+template <bool kFp8, int kWaves>
+__global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out, float* __restrict__ lse,
     const void* __restrict__ kpool, const void* __restrict__ vpool, const float* __restrict__ kscale,
     const float* __restrict__ vscale, const int32_t* __restrict__ block_tables, int32_t max_pages,
     int32_t num_reqs, int32_t hq, int32_t hkv, float scale_log2, PlanPtrs pv) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * kBufElems];
+  constexpr int kQuarters = kWaves / 4;              // waves sharing one page of a tile
+  constexpr int kRowsPerWave = 16 / kQuarters;       // key rows each wave moves per tile
+  constexpr int kDma = kRowsPerWave / 4;             // bf16: 1 KiB LDS-direct loads per wave
+  constexpr int kF8Loads = kRowsPerWave / 8;         // e4m3: 16-byte loads per lane
+  constexpr int kRun = kFp8 ? 16 * 128 : 16 * 128 * 2;   // bytes of one (page, kv head)
+  constexpr int kKeyBytes = kRun / 16;
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[kLdsBytes];
+
   const int W = pv.hdr->num_items;
   if ((int)blockIdx.x >= W) return;
   const int w_item = xcd_logical(blockIdx.x, gridDim.x < (unsigned)W ? gridDim.x : W);
@@ -238,7 +147,7 @@ __global__ __launch_bounds__(kThreads, kQB == 1 ? 2 : 1) void attn_main_kernel(
   const Item it = decode_local(w_item - pv.item_off[r], nqt, ns);
   const int P = pv.p[r], C = pv.c[r], row0 = pv.cu[r];
   const int G = hq / hkv;
-  const int tq = tile_tokens(G, 128 * kQB);
+  const int tq = tile_tokens(G, 32 * kWaves);
   const int i0 = it.qt * tq;
   const int i1 = min(i0 + tq, C);
   int lo, hi;
@@ -246,18 +155,14 @@ __global__ __launch_bounds__(kThreads, kQB == 1 ? 2 : 1) void attn_main_kernel(
   const int g = it.g;
   const int32_t* bt = block_tables + (int64_t)r * max_pages;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int n = lane & 31, half = lane >> 5;
-  int tok[kQB], hq_col[kQB], horizon[kQB];
-  bool valid[kQB];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const int col = (wave * kQB + qb) * 32 + n;
-    tok[qb] = i0 + col / G;
-    hq_col[qb] = g * G + col % G;
-    valid[qb] = col < tq * G && tok[qb] < i1;
-    horizon[qb] = valid[qb] ? P + tok[qb] : P + i1 - 1;   // last visible key of this column
-  }
+  const int col = wave * 32 + n;
+  const int tok = i0 + col / G;
+  const int hq_col = g * G + col % G;
+  const bool valid = col < tq * G && tok < i1;
+  const int horizon = valid ? P + tok : P + i1 - 1;   // last visible key of this column
 
   float c_log2 = scale_log2;
   float v_mul = 1.0f;
@@ -267,207 +172,426 @@ __global__ __launch_bounds__(kThreads, kQB == 1 ? 2 : 1) void attn_main_kernel(
   }
 
   // Q^T operand: lane (n, half) holds Q[col][16 ks + 8 half .. +7] for ks = 0..7.
-  bf16x8 qf[kQB][8];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const uint16_t* qrow =
-        q + ((int64_t)(row0 + (valid[qb] ? tok[qb] : 0)) * hq + (valid[qb] ? hq_col[qb] : 0)) * 128 + 8 * half;
+  bf16x8 qf[8];
+  {
+    const uint16_t* qrow = q + ((int64_t)(row0 + (valid ? tok : 0)) * hq + (valid ? hq_col : 0)) * 128 + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
-      u32x4 x = valid[qb] ? *reinterpret_cast<const u32x4*>(qrow + 16 * ks) : u32x4{0, 0, 0, 0};
-      qf[qb][ks] = __builtin_bit_cast(bf16x8, x);
+      u32x4 x = valid ? *reinterpret_cast<const u32x4*>(qrow + 16 * ks) : u32x4{0, 0, 0, 0};
+      qf[ks] = __builtin_bit_cast(bf16x8, x);
     }
   }
 
-  f32x16 o[kQB][4];
-  float m_run[kQB], l_run[kQB];
+  // LDS byte offsets of the operand reads, relative to a tile buffer.
+  // K (A of S^T = K Q^T), k-step ks, sub-block 0: row n, chunk 2 ks + half.
+  uint32_t ka[8];
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
+  for (int ks = 0; ks < 8; ++ks) ka[ks] = n * kRowBytes + ((((2 * ks + half) ^ (n & 15))) << 4);
+  // V^T (A of O^T += V^T P^T), d-block db, first 4-key set of k-step 0: within each group
+  // of 16 lanes, lane j addresses key row (j >> 2) at column 32 db + 16 ((l >> 4) & 1) +
+  // 4 (j & 3); the transposing read hands lane i the four keys of column base + i, so lane
+  // (n, half) receives V[keys 4 half + {0..3}, then (second read, +8 rows) 8 + 4 half +
+  // {0..3}][32 db + n]: the k-slot order of the score registers it multiplies.
+  uint32_t va[4];
+  {
+    const int j = lane & 15, b4 = (lane >> 4) & 1;
+    const int row = 4 * half + (j >> 2);
 #pragma unroll
-    for (int db = 0; db < 4; ++db) o[qb][db] = f32x16{};
-    m_run[qb] = 0.f;
-    l_run[qb] = 0.f;
+    for (int db = 0; db < 4; ++db)
+      va[db] = row * kRowBytes + ((4 * (db ^ ((j >> 2) & 3)) + 2 * b4 + ((j >> 1) & 1)) << 4) + 8 * (j & 1);
   }
+
+  // Tile loads: wave w moves rows [s0, s0 + kRowsPerWave) of page pw of each tile.
+  const int pw = wave / kQuarters;
+  const int s0 = (wave % kQuarters) * kRowsPerWave;
+  uint32_t kvo[kFp8 ? kF8Loads : kDma], vvo[kFp8 ? kF8Loads : kDma];
+  if constexpr (!kFp8) {
+    // LDS-direct load d writes tile rows 16 pw + s0 + 4d + (l >> 4), chunk l & 15: it
+    // fetches the source chunk that the row's permutation puts there.
+#pragma unroll
+    for (int d = 0; d < kDma; ++d) {
+      const int slot = s0 + 4 * d + (lane >> 4), c = lane & 15;
+      kvo[d] = slot * kRowBytes + ((c ^ slot) << 4);
+      vvo[d] = slot * kRowBytes + ((c ^ ((slot & 3) << 2)) << 4);
+    }
+  } else {
+    // lane l loads bytes [16 f, 16 f + 16) of key slot s0 + l / kLpr (f as below)
+#pragma unroll
+    for (int i = 0; i < kF8Loads; ++i) {
+      constexpr int kLpr = 8 / kF8Loads;
+      const int slot = s0 + lane / kLpr, f = (lane % kLpr) * kF8Loads + i;
+      kvo[i] = vvo[i] = slot * 128 + 16 * f;
+    }
+  }
+  const char* kpb = static_cast<const char*>(kpool) + (int64_t)g * kRun;
+  const char* vpb = static_cast<const char*>(vpool) + (int64_t)g * kRun;
+  const int64_t page_stride = (int64_t)hkv * kRun;
+
+  // Page pg of the tile at key kb into the K or V buffer at `dst` (bf16: LDS-direct).
+  struct F8Stage {
+    u32x4 x[kF8Loads];
+  };
+  auto dma_rows = [&](const char* base, int32_t pg, int kb, int dst, const uint32_t* vo, bool is_k) {
+    const int bytes = __builtin_amdgcn_readfirstlane(clamp16(hi - (kb + 16 * pw)) * kKeyBytes);
+    const i32x4 rs = sgpr_rsrc(base + (int64_t)pg * page_stride, bytes);
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)smem;
+#pragma unroll
+    for (int d = 0; d < kDma; ++d) {
+      const int row = 16 * pw + s0 + 4 * d;
+      lds_dma_b128(rs, vo[d], __builtin_amdgcn_readfirstlane(lds0 + dst + row * kRowBytes));
+    }
+    (void)is_k;
+  };
+  auto f8_load = [&](F8Stage& st, const char* base, int32_t pg, int kb, const uint32_t* vo) {
+    const int bytes = __builtin_amdgcn_readfirstlane(clamp16(hi - (kb + 16 * pw)) * kKeyBytes);
+    const auto rs = make_rsrc(base + (int64_t)pg * page_stride, bytes);
+#pragma unroll
+    for (int i = 0; i < kF8Loads; ++i)
+      st.x[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, vo[i], 0, 0));
+  };
+  // e4m3 -> bf16 into the permuted rows: 16 codes = bf16 chunks 2f, 2f + 1.
+  auto f8_store = [&](const F8Stage& st, int dst, bool is_k) {
+#pragma unroll
+    for (int i = 0; i < kF8Loads; ++i) {
+      constexpr int kLpr = 8 / kF8Loads;
+      const int row = 16 * pw + s0 + lane / kLpr, f = (lane % kLpr) * kF8Loads + i;
+      const int sw = is_k ? (row & 15) : ((row & 3) << 2);
+      const u32x2 a = fp8x4_to_bf16x4(st.x[i][0]);
+      const u32x2 b = fp8x4_to_bf16x4(st.x[i][1]);
+      const u32x2 c = fp8x4_to_bf16x4(st.x[i][2]);
+      const u32x2 d = fp8x4_to_bf16x4(st.x[i][3]);
+      uint8_t* rp = smem + dst + row * kRowBytes;
+      *reinterpret_cast<u32x4*>(rp + (((2 * f) ^ sw) << 4)) = u32x4{a[0], a[1], b[0], b[1]};
+      *reinterpret_cast<u32x4*>(rp + (((2 * f + 1) ^ sw) << 4)) = u32x4{c[0], c[1], d[0], d[1]};
+    }
+  };
+
+  f32x16 o[4];
+#pragma unroll
+  for (int db = 0; db < 4; ++db) o[db] = f32x16{};
+  // Row sums per lane: b sums the bf16 probabilities exactly as P.V uses them (O is
+  // normalised by it), f sums them unrounded in fp32 (the log-sum-exp).
+  struct Sums {
+    float b, f;
+  };
+  float m_run = 0.f;
+  Sums l_run = {0.f, 0.f};
+
+  // S(b+1) = K(b+1) Q^T from the sub-block at LDS byte `kofs`.
+  auto qk = [&](int kofs) {
+    f32x16 s = f32x16{};
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(smem + kofs + ka[ks]);
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s, 0, 0, 0);
+    }
+    return s;
+  };
+  // O += P V over the sub-block whose V rows start at LDS byte `vofs`.
+  auto pv_acc = [&](const u32x4* p, int vofs) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, p[k2]);
+#pragma unroll
+      for (int db = 0; db < 4; ++db) {
+        const uint8_t* base = smem + vofs + 16 * k2 * kRowBytes + va[db];
+        const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base));
+        const v4i16 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + 8 * kRowBytes));
+        const u32x2 ux = __builtin_bit_cast(u32x2, x), uy = __builtin_bit_cast(u32x2, y);
+        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{ux[0], ux[1], uy[0], uy[1]});
+        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[db], 0, 0, 0);
+      }
+    }
+  };
+  // One A fragment of O^T += V^T P^T: keys 16 k2 + (4-key sets of this lane half), d-block db.
+  auto read_v = [&](int vofs, int k2, int db) {
+    const uint8_t* base = smem + vofs + 16 * k2 * kRowBytes + va[db];
+    const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base));
+    const v4i16 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + 8 * kRowBytes));
+    const u32x2 ux = __builtin_bit_cast(u32x2, x), uy = __builtin_bit_cast(u32x2, y);
+    return __builtin_bit_cast(bf16x8, u32x4{ux[0], ux[1], uy[0], uy[1]});
+  };
+  auto read_k = [&](int kofs, int ks) { return *reinterpret_cast<const bf16x8*>(smem + kofs + ka[ks]); };
+  // Operands of a step's first two slots, read before its (branchy) softmax prologue.
+  struct Pre {
+    bf16x8 k[2], v[2];
+  };
+  auto prefetch = [&](int kofs, int vofs, auto with_qk) {
+    Pre f;
+    if constexpr (decltype(with_qk)::value) {
+      f.k[0] = read_k(kofs, 0);
+      f.k[1] = read_k(kofs, 1);
+    }
+    f.v[0] = read_v(vofs, 0, 0);
+    f.v[1] = read_v(vofs, 0, 1);
+    return f;
+  };
+  // Pipelined step in eight slots; slot i issues S(b+1) += K_i Q_i (k-step i), O_db +=
+  // V^T P(b-1) (k2 = i / 4, db = i % 4) and the probabilities of score elements 2i, 2i+1
+  // of sub-block b, while the operands of slot i + 2 are read from LDS.
+  auto step_main = [&](const f32x16& s, const u32x4* pp, u32x4* po, int kofs, int vofs, const Pre& f,
+                       auto with_qk, Sums& lsum) {
+    constexpr bool kQK = decltype(with_qk)::value;
+    f32x16 sn = f32x16{};
+    bf16x8 kf[10], vf[10];
+    kf[0] = f.k[0];
+    kf[1] = f.k[1];
+    vf[0] = f.v[0];
+    vf[1] = f.v[1];
+    float l0 = 0.f, l1 = 0.f, f0 = 0.f, f1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (i + 2 < 8) {
+        if constexpr (kQK) kf[i + 2] = read_k(kofs, i + 2);
+        vf[i + 2] = read_v(vofs, (i + 2) >> 2, (i + 2) & 3);
+      }
+      if constexpr (kQK) sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i], qf[i], sn, 0, 0, 0);
+      o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], __builtin_bit_cast(bf16x8, pp[i >> 2]), o[i & 3],
+                                                          0, 0, 0);
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * i], c_log2, -m_run));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * i + 1], c_log2, -m_run));
+      const uint32_t pk = pack_bf16x2(p0, p1);
+      po[i >> 2][i & 3] = pk;
+      if (i & 1) {
+        l1 = sum_bf16x2(pk, l1);
+        f1 += p0 + p1;
+      } else {
+        l0 = sum_bf16x2(pk, l0);
+        f0 += p0 + p1;
+      }
+    }
+    lsum = Sums{l0 + l1, f0 + f1};
+    __asm__ volatile("" ::"v"(po[0]), "v"(po[1]), "v"(lsum.b), "v"(lsum.f));   // produced here, not sunk
+    slot_schedule<kQK, true>();
+    slot_schedule<kQK, true>();
+    slot_schedule<kQK, true>();
+    slot_schedule<kQK, true>();
+    slot_schedule<kQK, true>();
+    slot_schedule<kQK, true>();
+    slot_schedule<kQK, false>();
+    slot_schedule<kQK, false>();
+    return sn;
+  };
+  // Causal mask of sub-block sb0 (element e of a lane's scores is key sb0 + 8 (e / 4) +
+  // 4 half + e % 4), applied only where the sub-block reaches past the first query token.
+  auto mask = [&](f32x16& s, int sb0) {
+    if (sb0 + 31 > P + i0) {
+      __asm__ volatile("" ::);   // keep this a branch (not predicated into every sub-block)
+      const int lim = horizon - sb0 - 4 * half;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) s[e] = 8 * (e >> 2) + (e & 3) > lim ? -INFINITY : s[e];
+    }
+  };
+  // exp2(s c - m) -> bf16 pairs (k-slot order of the B operand) and both row sums.
+  auto probs = [&](const f32x16& s, u32x4* p, Sums& lsum) {
+    float l0 = 0.f, l1 = 0.f, f0 = 0.f, f1 = 0.f;
+#pragma unroll
+    for (int e = 0; e < 16; e += 4) {
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c_log2, -m_run));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e + 1], c_log2, -m_run));
+      const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e + 2], c_log2, -m_run));
+      const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e + 3], c_log2, -m_run));
+      const uint32_t pk0 = pack_bf16x2(p0, p1), pk1 = pack_bf16x2(p2, p3);
+      p[e >> 3][(e >> 1) & 3] = pk0;
+      p[e >> 3][((e >> 1) & 3) + 1] = pk1;
+      l0 = sum_bf16x2(pk0, l0);
+      l1 = sum_bf16x2(pk1, l1);
+      f0 += p0 + p1;
+      f1 += p2 + p3;
+    }
+    lsum = Sums{l0 + l1, f0 + f1};
+  };
+  // Settles the probabilities P of the previous sub-block (scores s, row sum lsum) before
+  // they enter O.  They were computed against the running reference m; only when one of
+  // them exceeds 2^64 (seen in the row sum, an overflow to inf included) is the column's
+  // reference raised to that sub-block's exact max: O and l, which hold only earlier
+  // sub-blocks, are rescaled and P is recomputed (rare branch).  Then the sum joins l.  The
+  // reference of a column is shared by its lane pair, and so is the decision.
+  auto settle = [&](const f32x16& s, u32x4* p, Sums& lsum) {
+    if (__builtin_amdgcn_ballot_w64(lsum.f > kOverflow) != 0) {
+      __asm__ volatile("" ::);
+      const bool over = max_with_partner(lsum.f) > kOverflow;
+      const float t = block_max(s) * c_log2;
+      const float m_new = over ? t : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+#pragma unroll
+      for (int db = 0; db < 4; ++db) o[db] *= alpha;
+      l_run.b *= alpha;
+      l_run.f *= alpha;
+      m_run = m_new;
+      probs(s, p, lsum);
+    }
+    l_run.b += lsum.b;
+    l_run.f += lsum.f;
+  };
 
   const int ntiles = hi > lo ? ceil_div(hi - lo, kKvTile) : 0;
-  bool first = true;   // wave-uniform: the next sub-block is the item's first
   const int last_page = hi > lo ? (hi - 1) >> 4 : 0;
-  Stage st;
-  int32_t page_next = 0;   // (vector) page-id entry of the tile after the one being loaded
-  const LoadOffsets loff = load_offsets<kFp8>();
-  const uint32_t page_lane_off = 4u * (threadIdx.x & 3);
-  const char* kpb = static_cast<const char*>(kpool);
-  const char* vpb = static_cast<const char*>(vpool);
+  const int P_i0 = P + i0;
+  (void)P_i0;
+
+  auto load_k = [&](int t, int32_t pg, int buf) {  // K of tile t into K buffer buf
+    if constexpr (!kFp8) dma_rows(kpb, pg, lo + t * kKvTile, kKBuf + buf * kTileBytes, kvo, true);
+  };
+  auto load_v = [&](int t, int32_t pg, int buf) {
+    if constexpr (!kFp8) dma_rows(vpb, pg, lo + t * kKvTile, kVBuf + buf * kTileBytes, vvo, false);
+  };
+
+  f32x16 sp, sc;                 // scores of the previous and the current sub-block
+  u32x4 pa[2], pb[2];
+  Sums lsum_p = {0.f, 0.f};      // row sums of the probabilities not yet settled
+  int32_t pg_next_v = 0;       // page (this wave's) of the tile whose V is loaded next
+  int32_t pid_v = 0;           // vector copy of a page-table entry loaded ahead
+  F8Stage kst, vst;
+
   if (ntiles > 0) {
-    const Pages pg0 = broadcast_pages(tile_page_entry(bt, lo, last_page, page_lane_off));
-    load_tile<kFp8>(st, kpb, vpb, pg0, g, hkv, loff);
-    if (ntiles > 1) page_next = tile_page_entry(bt, lo + kKvTile, last_page, page_lane_off);
-    if (lo + kKvTile > hi) mask_tile<kFp8>(st, lo, hi);
-    store_tile<kFp8>(st, smem);
-  }
-  // Nothing loaded before the loop may remain in flight at its head: otherwise the compiler's
-  // wait-count bookkeeping, merging the entry and back edges, puts a full wait for vector
-  // loads in front of every iteration's first MFMA, serialising the prefetch.
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-
-  for (int ti = 0; ti < ntiles; ++ti) {
-    const int kb0 = lo + ti * kKvTile;
-    const uint16_t* kl = smem + (ti & 1) * kBufElems;
-    const uint16_t* vl = kl + kKTile;
-    const bool more = ti + 1 < ntiles;
-    if (more) {
-      const int kb1 = kb0 + kKvTile;
-      const Pages pg = broadcast_pages(page_next);
-      if (ti + 2 < ntiles) page_next = tile_page_entry(bt, kb1 + kKvTile, last_page, page_lane_off);
-      load_tile<kFp8>(st, kpb, vpb, pg, g, hkv, loff);
-    }
-
-    // S^T = K Q^T for both 32-key sub-blocks (two independent MFMA chains); element e of
-    // sc[kb][qb] is key kb0 + 32 kb + 8(e/4) + 4 half + e%4.  Softmax and P.V then run one
-    // sub-block at a time.
-    f32x16 sc[2][kQB];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int qb = 0; qb < kQB; ++qb) sc[kb][qb] = f32x16{};
-#pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bf16x8 a = *reinterpret_cast<const bf16x8*>(kl + (32 * kb + n) * kKRow + 16 * ks + 8 * half);
-#pragma unroll
-        for (int qb = 0; qb < kQB; ++qb)
-          sc[kb][qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[qb][ks], sc[kb][qb], 0, 0, 0);
-      }
-    }
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16* s = sc[kb];
-
-      // Online softmax in the log2 domain against the running reference m_run: x = s c - m.
-      // The reference is set on the item's first sub-block and afterwards only raised when a
-      // score exceeds it by more than 2^8 (probabilities up to 2^8 are accumulated against a
-      // stale reference; the final division makes the result exact).  A lane whose first
-      // sub-block is fully masked sees no key in the whole piece (its keys only grow), so its
-      // reference can stay unset.
-      const int sb0 = kb0 + 32 * kb;
-      float xmax[kQB];
-      bool over = false;
-#pragma unroll
-      for (int qb = 0; qb < kQB; ++qb) {
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[qb][e] = __builtin_fmaf(s[qb][e], c_log2, -m_run[qb]);
-      }
-      if (sb0 + 31 > P + i0) {   // chunk-diagonal sub-block: causal mask
-        __asm__ volatile("" ::);  // keep this a branch (not predicated into every sub-block)
-#pragma unroll
-        for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int key = sb0 + 8 * (e >> 2) + 4 * half + (e & 3);
-            s[qb][e] = key > horizon[qb] ? -INFINITY : s[qb][e];
-          }
-      }
-#pragma unroll
-      for (int qb = 0; qb < kQB; ++qb) {
-        float mx = vmax3(s[qb][0], s[qb][1], s[qb][2]);
-#pragma unroll
-        for (int e = 3; e < 15; e += 2) mx = vmax3(mx, s[qb][e], s[qb][e + 1]);
-        mx = vmax2(mx, s[qb][15]);
-        xmax[qb] = max_with_partner(mx);
-        over |= xmax[qb] > kRescaleSlack;
-      }
-      if (first || __any(over)) {
-        __asm__ volatile("" ::);
-#pragma unroll
-        for (int qb = 0; qb < kQB; ++qb) {
-          // new reference: the block maximum (first block) or the larger of old and new
-          const float cand = xmax[qb] + m_run[qb];
-          const float m_new = xmax[qb] == -INFINITY ? m_run[qb] : (first ? cand : fmaxf(m_run[qb], cand));
-          const float alpha = first ? 0.0f : __builtin_amdgcn_exp2f(m_run[qb] - m_new);
-          const float shift = m_new - m_run[qb];
-          m_run[qb] = m_new;
-          l_run[qb] *= alpha;
-#pragma unroll
-          for (int db = 0; db < 4; ++db) o[qb][db] *= alpha;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) s[qb][e] -= shift;
-        }
-        first = false;
-      }
-      uint32_t pk[kQB][8];
-#pragma unroll
-      for (int qb = 0; qb < kQB; ++qb) {
-        float lsum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; e += 2) {
-          const float p0 = __builtin_amdgcn_exp2f(s[qb][e]);
-          const float p1 = __builtin_amdgcn_exp2f(s[qb][e + 1]);
-          lsum += p0 + p1;
-          pk[qb][e >> 1] = pack_bf16x2(p0, p1);
-        }
-        l_run[qb] += lsum;
-      }
-
-      // O^T += V^T P^T over the sub-block's two k-steps of 16 keys.
-#pragma unroll
-      for (int k2 = 0; k2 < 2; ++k2) {
-        const int ks = 2 * kb + k2;
-        bf16x8 pb[kQB];
-#pragma unroll
-        for (int qb = 0; qb < kQB; ++qb)
-          pb[qb] = __builtin_bit_cast(bf16x8, u32x4{pk[qb][4 * k2], pk[qb][4 * k2 + 1], pk[qb][4 * k2 + 2],
-                                                    pk[qb][4 * k2 + 3]});
-#pragma unroll
-        for (int db = 0; db < 4; ++db) {
-          const bf16x8 a = read_vt(vl, ks, db);
-#pragma unroll
-          for (int qb = 0; qb < kQB; ++qb)
-            o[qb][db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[qb], o[qb][db], 0, 0, 0);
-        }
-      }
-    }
-    if (more) {
-      if (kb0 + 2 * kKvTile > hi) mask_tile<kFp8>(st, kb0 + kKvTile, hi);
-      store_tile<kFp8>(st, smem + ((ti + 1) & 1) * kBufElems);
-    }
-    __syncthreads();
-  }
-
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const float l_tot = sum_with_partner(l_run[qb]);
-    if (!valid[qb]) continue;
-    if (ns == 1) {
-      const float inv = v_mul / l_tot;
-      uint16_t* orow = out + ((int64_t)(row0 + tok[qb]) * hq + hq_col[qb]) * 128 + 4 * half;
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const u32x2 w = {pack_bf16x2(o[qb][db][4 * j] * inv, o[qb][db][4 * j + 1] * inv),
-                           pack_bf16x2(o[qb][db][4 * j + 2] * inv, o[qb][db][4 * j + 3] * inv)};
-          *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * j) = w;
-        }
-      if (lse != nullptr && half == 0)
-        lse[(int64_t)(row0 + tok[qb]) * hq + hq_col[qb]] = (m_run[qb] + __log2f(l_tot)) * kLn2;
+    const int e0 = table_entry(bt, (lo >> 4) + pw, last_page);
+    const int e1 = ntiles > 1 ? table_entry(bt, ((lo + kKvTile) >> 4) + pw, last_page) : 0;
+    if (ntiles > 2) pid_v = table_entry(bt, ((lo + 2 * kKvTile) >> 4) + pw, last_page);
+    __builtin_amdgcn_s_waitcnt(0);
+    const int32_t pg0 = __builtin_amdgcn_readfirstlane(e0);
+    const int32_t pg1 = __builtin_amdgcn_readfirstlane(e1);
+    if constexpr (!kFp8) {
+      load_k(0, pg0, 0);
+      load_v(0, pg0, 0);
+      if (ntiles > 1) load_k(1, pg1, 1);
     } else {
-      float* acc = pv.partials + pv.part_off[r];
-      float* ml = acc + (int64_t)ns * C * hq * kHeadDim;
-      const int64_t prow = ((int64_t)it.s * C + tok[qb]) * hq + hq_col[qb];
-      float* arow = acc + prow * kHeadDim + 4 * half;
-#pragma unroll
-      for (int db = 0; db < 4; ++db)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const f32x4 w = {o[qb][db][4 * j] * v_mul, o[qb][db][4 * j + 1] * v_mul, o[qb][db][4 * j + 2] * v_mul,
-                           o[qb][db][4 * j + 3] * v_mul};
-          *reinterpret_cast<f32x4*>(arow + 32 * db + 8 * j) = w;
-        }
-      // a column with no visible key in this piece: (m, l) = (-inf, 0), skipped by the merge
-      if (half == 0) *reinterpret_cast<f32x2*>(ml + 2 * prow) = f32x2{l_tot > 0.f ? m_run[qb] : -INFINITY, l_tot};
+      f8_load(kst, kpb, pg0, lo, kvo);
+      f8_load(vst, vpb, pg0, lo, vvo);
+      __builtin_amdgcn_s_waitcnt(0);
+      f8_store(kst, kKBuf, true);
+      f8_store(vst, kVBuf, false);
+      if (ntiles > 1) {
+        f8_load(kst, kpb, pg1, lo + kKvTile, kvo);
+        __builtin_amdgcn_s_waitcnt(0);
+        f8_store(kst, kKBuf + kTileBytes, true);
+      }
     }
+    pg_next_v = pg1;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+
+    // Sub-block 0 sets the reference to its own max (a lane with no visible key there has
+    // none in the whole piece, as its visible keys form a prefix of the range).
+    sp = qk(kKBuf);
+    mask(sp, lo);
+    {
+      const float t = block_max(sp) * c_log2;
+      m_run = t == -INFINITY ? 0.f : t;
+    }
+    probs(sp, pa, lsum_p);
+    sc = qk(kKBuf + kSubBytes);
+    __syncthreads();   // K tile 0 is overwritten by the first iteration's loads
+  }
+
+  // Iteration t: loads K(t + 2), V(t + 1); sub-blocks 2t+1 and 2t+2 take the softmax, their
+  // successors S from K(t + 1), their predecessors O += P V from V(t).  kPar = t & 1.
+  auto iteration = [&](int t, auto par) {
+    constexpr int kPar = decltype(par)::value;
+    const int kcur = kKBuf + (kPar ^ 1) * kTileBytes;   // K(t + 1)
+    const int vcur = kVBuf + kPar * kTileBytes;         // V(t)
+    const int32_t pg_v = pg_next_v;
+    if (t + 2 < ntiles) {
+      const int32_t pg_k = __builtin_amdgcn_readfirstlane(pid_v);
+      if (t + 3 < ntiles) pid_v = table_entry(bt, ((lo + (t + 3) * kKvTile) >> 4) + pw, last_page);
+      if constexpr (!kFp8) load_k(t + 2, pg_k, kPar);
+      else f8_load(kst, kpb, pg_k, lo + (t + 2) * kKvTile, kvo);
+      pg_next_v = pg_k;
+    }
+    if constexpr (!kFp8) load_v(t + 1, pg_v, kPar ^ 1);
+    else f8_load(vst, vpb, pg_v, lo + (t + 1) * kKvTile, vvo);
+
+    const int sb1 = lo + (2 * t + 1) * 32;
+    constexpr std::true_type kWithQK{};
+    // sub-block 2t+1 (scores sc; P(2t) in pa, from scores sp)
+    {
+      const Pre f = prefetch(kcur, vcur, kWithQK);
+      settle(sp, pa, lsum_p);
+      mask(sc, sb1);
+      Sums ls;
+      const f32x16 sn = step_main(sc, pa, pb, kcur, vcur, f, kWithQK, ls);
+      sp = sc;
+      sc = sn;
+      lsum_p = ls;
+    }
+    // sub-block 2t+2 (P(2t+1) in pb)
+    {
+      const Pre f = prefetch(kcur + kSubBytes, vcur + kSubBytes, kWithQK);
+      settle(sp, pb, lsum_p);
+      mask(sc, sb1 + 32);
+      Sums ls;
+      const f32x16 sn = step_main(sc, pb, pa, kcur + kSubBytes, vcur + kSubBytes, f, kWithQK, ls);
+      sp = sc;
+      sc = sn;
+      lsum_p = ls;
+    }
+    if constexpr (kFp8) {
+      __builtin_amdgcn_s_waitcnt(0);
+      if (t + 2 < ntiles) f8_store(kst, kKBuf + kPar * kTileBytes, true);
+      f8_store(vst, kVBuf + (kPar ^ 1) * kTileBytes, false);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  };
+
+  // Every load issued so far is complete here on every path (also ntiles == 0, which skips
+  // the block above): otherwise the compiler's bookkeeping keeps the Q loads pending at the
+  // loop head and waits for all vector memory, LDS-direct copies included, in each step.
+  __builtin_amdgcn_s_waitcnt(0);
+  int t = 0;
+  for (; t + 2 < ntiles; t += 2) {
+    iteration(t, std::integral_constant<int, 0>{});
+    iteration(t + 1, std::integral_constant<int, 1>{});
+  }
+  if (t + 1 < ntiles) {
+    iteration(t, std::integral_constant<int, 0>{});
+    ++t;
+  }
+  if (ntiles > 0) {
+    // last tile (t = ntiles - 1): sub-block 2t+1 takes the softmax, P(2t) V, then P(2t+1) V
+    const int vlast = kVBuf + (t & 1) * kTileBytes;
+    constexpr std::false_type kNoQK{};
+    const Pre f = prefetch(0, vlast, kNoQK);
+    settle(sp, pa, lsum_p);
+    mask(sc, lo + (2 * t + 1) * 32);
+    Sums ls;
+    step_main(sc, pa, pb, 0, vlast, f, kNoQK, ls);
+    settle(sc, pb, ls);
+    pv_acc(pb, vlast + kSubBytes);
+  }
+
+  const float lb_tot = sum_with_partner(l_run.b);
+  const float lf_tot = sum_with_partner(l_run.f);
+  if (!valid) return;
+  if (ns == 1) {
+    const float inv = v_mul / lb_tot;
+    uint16_t* orow = out + ((int64_t)(row0 + tok) * hq + hq_col) * 128 + 4 * half;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const u32x2 w = {pack_bf16x2(o[db][4 * j] * inv, o[db][4 * j + 1] * inv),
+                         pack_bf16x2(o[db][4 * j + 2] * inv, o[db][4 * j + 3] * inv)};
+        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * j) = w;
+      }
+    if (lse != nullptr && half == 0) lse[(int64_t)(row0 + tok) * hq + hq_col] = (m_run + __log2f(lf_tot)) * kLn2;
+  } else {
+    float* acc = pv.partials + pv.part_off[r];
+    float* ml = acc + (int64_t)ns * C * hq * kHeadDim;
+    const int64_t prow = ((int64_t)it.s * C + tok) * hq + hq_col;
+    float* arow = acc + prow * kHeadDim + 4 * half;
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 w = {o[db][4 * j] * v_mul, o[db][4 * j + 1] * v_mul, o[db][4 * j + 2] * v_mul,
+                         o[db][4 * j + 3] * v_mul};
+        *reinterpret_cast<f32x4*>(arow + 32 * db + 8 * j) = w;
+      }
+    // (m, l_b, l_f, 0); a column with no visible key in this piece has (-inf, 0, 0): the
+    // merge skips it
+    if (half == 0)
+      *reinterpret_cast<f32x4*>(ml + 4 * prow) = f32x4{lf_tot > 0.f ? m_run : -INFINITY, lb_tot, lf_tot, 0.f};
   }
 }
 
@@ -488,30 +612,31 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(uint16_t* __restrict_
   if (u < hq * 32) {
     const int h = u >> 5, d4 = (u & 31) * 4;
     float mstar = -INFINITY;
-    for (int s = 0; s < ns; ++s) mstar = fmaxf(mstar, ml[2 * (((int64_t)s * C + tok) * hq + h)]);
-    float lstar = 0.f;
+    for (int s = 0; s < ns; ++s) mstar = fmaxf(mstar, ml[4 * (((int64_t)s * C + tok) * hq + h)]);
+    float lb = 0.f, lf = 0.f;
     f32x4 a = {0.f, 0.f, 0.f, 0.f};
     for (int s = 0; s < ns; ++s) {
       const int64_t prow = ((int64_t)s * C + tok) * hq + h;
-      const float ms = ml[2 * prow];
-      if (ms == -INFINITY) continue;
-      const float wgt = __builtin_amdgcn_exp2f(ms - mstar);
-      lstar += wgt * ml[2 * prow + 1];
+      const f32x4 mlp = *reinterpret_cast<const f32x4*>(ml + 4 * prow);
+      if (mlp[0] == -INFINITY) continue;
+      const float wgt = __builtin_amdgcn_exp2f(mlp[0] - mstar);
+      lb += wgt * mlp[1];
+      lf += wgt * mlp[2];
       const f32x4 x = *reinterpret_cast<const f32x4*>(acc + prow * kHeadDim + d4);
       a += wgt * x;
     }
-    const float inv = 1.0f / lstar;
+    const float inv = 1.0f / lb;
     const u32x2 w = {pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv)};
     *reinterpret_cast<u32x2*>(out + ((int64_t)row * hq + h) * kHeadDim + d4) = w;
-    if (lse != nullptr && d4 == 0) lse[(int64_t)row * hq + h] = (mstar + __log2f(lstar)) * kLn2;
+    if (lse != nullptr && d4 == 0) lse[(int64_t)row * hq + h] = (mstar + __log2f(lf)) * kLn2;
   }
 }
 
 }  // namespace
 
-template <bool kFp8, int kQB>
+template <bool kFp8, int kWaves>
 void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
-  attn_main_kernel<kFp8, kQB><<<a.num_items, kThreads, 0, stream>>>(
+  attn_main_kernel<kFp8, kWaves><<<a.num_items, kWaves * 64, 0, stream>>>(
       static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
       a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.kv.num_reqs, a.hq, a.kv.hkv,
       a.softmax_scale * kLog2e, plan_ptrs(a.workspace, a.kv.num_reqs));
@@ -521,11 +646,11 @@ hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream) {
   if (a.num_items <= 0) return hipSuccess;
   const bool wide = a.tile_cols == kMaxTileCols;
   if (a.kv.fp8) {
-    if (wide) launch_main_variant<true, 2>(a, stream);
-    else launch_main_variant<true, 1>(a, stream);
+    if (wide) launch_main_variant<true, 8>(a, stream);
+    else launch_main_variant<true, 4>(a, stream);
   } else {
-    if (wide) launch_main_variant<false, 2>(a, stream);
-    else launch_main_variant<false, 1>(a, stream);
+    if (wide) launch_main_variant<false, 8>(a, stream);
+    else launch_main_variant<false, 4>(a, stream);
   }
   return hipGetLastError();
 }

@@ -22,7 +22,7 @@ namespace s2l {
 constexpr int kHeadDim = 128;
 constexpr int kPageSize = 16;
 constexpr int kMinTileCols = 128;   // packed (token, head) columns per work item: 4 waves x 32
-constexpr int kMaxTileCols = 256;   //   or 4 waves x 64
+constexpr int kMaxTileCols = 256;   //   or 8 waves x 32
 constexpr int kKvTile = 64;         // keys per LDS tile
 constexpr int kMaxSplitsCap = 64;
 constexpr int kDefaultMinSplitKeys = 512;
@@ -92,9 +92,10 @@ S2L_HD inline void piece_range(int32_t kv_end, int32_t ns, int32_t s, int32_t* l
   *hi = b > a ? b : a;
 }
 
-// Floats of split partials for one request: ns pieces x C rows x Hq heads x (D + 2).
+// Floats of split partials for one request: ns pieces x C rows x Hq heads x (D + 4): the
+// unnormalised output row, then (m, l_b, l_f, 0) per row.
 S2L_HD inline int64_t req_part_floats(int32_t ns, int32_t c, int32_t hq) {
-  return ns > 1 ? (int64_t)ns * c * hq * (kHeadDim + 2) : 0;
+  return ns > 1 ? (int64_t)ns * c * hq * (kHeadDim + 4) : 0;
 }
 
 // Workspace layout (byte offsets), a function of R only.

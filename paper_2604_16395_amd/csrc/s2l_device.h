@@ -44,31 +44,34 @@ __device__ inline uint32_t f32x4_to_fp8x4(float a, float b, float c, float d) {
   return w;
 }
 
+// acc + lo + hi of a packed bf16 pair, in fp32 (v_dot2_f32_bf16 with (1, 1)).
+__device__ inline float sum_bf16x2(uint32_t w, float acc) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, w), __builtin_bit_cast(bf16x2, 0x3F803F80u), acc,
+                                         false);
+}
+
 __device__ inline float bf16lo(uint32_t w) { return u2f(w << 16); }
 __device__ inline float bf16hi(uint32_t w) { return u2f(w & 0xFFFF0000u); }
 
-// IEEE max of three / two values as single VALU instructions.  Plain fmaxf() makes the
-// compiler canonicalise each operand first (one extra v_max per value) whenever it cannot
-// prove the operand canonical; the values here are never signalling NaNs.
-__device__ inline float vmax3(float a, float b, float c) {
-  float r;
-  __asm__("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
-__device__ inline float vmax2(float a, float b) {
-  float r;
-  __asm__("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
-  return r;
-}
-
-// Exchange with lane l ^ 32 (v_permlane32_swap): r[0], r[1] are {own, partner} in some order.
+// Combination over the lane pair (l, l ^ 32) with v_permlane32_swap, written as one
+// assembly block: the compiler treats the two results of permlane32_swap(x, x) as equal and
+// folds max(r0, r1) to r0 and r0 + r1 to 2 r0.  The s_nops keep the swap's operand reads
+// and the combining read apart from the VALU writes before them.  The input must come from
+// an ordinary VALU instruction (not an MFMA or a transcendental), whose hazards are the
+// only ones these wait states cover.
 __device__ inline float max_with_partner(float x) {
-  auto r = __builtin_amdgcn_permlane32_swap(f2u(x), f2u(x), false, false);
-  return vmax2(u2f(r[0]), u2f(r[1]));
+  float y;
+  __asm__("s_nop 1\n\tv_mov_b32 %1, %0\n\ts_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1\n\t"
+          "v_max_f32 %0, %0, %1"
+          : "+v"(x), "=&v"(y));
+  return x;
 }
 __device__ inline float sum_with_partner(float x) {
-  auto r = __builtin_amdgcn_permlane32_swap(f2u(x), f2u(x), false, false);
-  return u2f(r[0]) + u2f(r[1]);
+  float y;
+  __asm__("s_nop 1\n\tv_mov_b32 %1, %0\n\ts_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1\n\t"
+          "v_add_f32 %0, %0, %1"
+          : "+v"(x), "=&v"(y));
+  return x;
 }
 
 }  // namespace s2l

@@ -189,7 +189,27 @@ def test_weighted_abs_values_are_the_same_weights_on_abs_v():
     rng = np.random.default_rng(8)
     P, C, d = 30, 9, 16
     q, k, v = _rand(rng, C, 4, d), _rand(rng, P + C, 2, d), _rand(rng, P + C, 2, d)
-    o, l, oa = ref_chunk_attn_blocked(q, k, v, P, 0.3, k_block=7, with_abs=True)
+    o, l, oa, od = ref_chunk_attn_blocked(q, k, v, P, 0.3, k_block=7, with_abs=True)
     o2, _ = ref_chunk_attn_blocked(q, k, np.abs(v), P, 0.3)
     assert np.allclose(oa, o2, rtol=1e-13, atol=0)
     assert np.all(oa >= np.abs(o) - 1e-15)
+    # B = sum_j w_j |V_j - O| from the softmax weights written out one row at a time
+    for i in (0, 4, C - 1):
+        for h in range(4):
+            keys = np.arange(P + i + 1)
+            s = np.array([0.3 * float(q[i, h] @ k[j, h // 2]) for j in keys])
+            w = np.exp(s - s.max())
+            w /= w.sum()
+            dev = (w[:, None] * np.abs(v[keys, h // 2] - o[i, h][None, :])).sum(axis=0)
+            assert np.allclose(od[i, h], dev, rtol=1e-12, atol=1e-15)
+    assert np.all(od >= 0) and np.all(od <= oa + np.abs(o) + 1e-12)
+
+
+def test_weighted_deviation_is_zero_when_all_values_agree():
+    rng = np.random.default_rng(9)
+    P, C, d = 20, 5, 8
+    q, k = _rand(rng, C, 2, d), _rand(rng, P + C, 1, d)
+    v = np.broadcast_to(_rand(rng, 1, 1, d), (P + C, 1, d)).copy()
+    o, _, oa, od = ref_chunk_attn_blocked(q, k, v, P, 0.5, k_block=6, with_abs=True)
+    assert np.allclose(o, v[0, 0][None, None, :], rtol=1e-13, atol=1e-15)
+    assert np.all(od < 1e-13)
