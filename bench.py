@@ -9,7 +9,9 @@ pages from HBM rather than from the 256 MB last-level cache, as a 32-layer model
 
 Prints ONE JSON line.  `value` is algorithmic TFLOP/s of the whole step (4*d*Hq FLOPs per
 query/visible-key pair, unmasked pairs only) with every input already resident in HBM.
-`roofline` reports the attention kernel alone, timed with HIP events on its own stream.
+`roofline` reports the attention kernel alone: its average launch duration over graphs of
+back-to-back launches, timed with HIP events on the stream it runs on.  All launches are
+captured into HIP graphs once and replayed, so the timed regions measure the GPU.
 `cpu_baseline` times the fp64 oracle on this machine's host cores.
 """
 import argparse
@@ -97,6 +99,8 @@ def main():
     ap.add_argument("--chunk", type=int, default=512)
     ap.add_argument("--layers", type=int, default=32, help="KV pool copies rotated over the steps")
     ap.add_argument("--tile-cols", type=int, default=0, help="query columns per work item (0 = library default)")
+    ap.add_argument("--key-halves", type=int, default=0,
+                    help="wave groups per work item splitting its key range (0 = library default)")
     ap.add_argument("--target-items", type=int, default=0,
                     help="work items the planner aims for when splitting prefixes (0 = library default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -150,56 +154,85 @@ def main():
     v_new = bf16(case.new_rows(case.v_full_bits))
     out = torch.empty((C, HQ, 128), dtype=torch.bfloat16, device=dev)
     lse = torch.empty((C, HQ), dtype=torch.float32, device=dev)
-    opts = s2l.plan_opts(tile_cols=args.tile_cols, target_items=args.target_items)
+    opts = s2l.plan_opts(tile_cols=args.tile_cols, key_halves=args.key_halves, target_items=args.target_items)
     ws = torch.empty(s2l.s2l_attn_workspace_bytes(batch, HQ, HKV, opts), dtype=torch.uint8, device=dev)
     scale = 1.0 / np.sqrt(128.0)
-    stream = torch.cuda.Stream()
+    main_stream = torch.cuda.Stream()
     torch.cuda.synchronize()
 
-    def step(i, ev=None):
-        cache = caches[i % L]
-        if ev is not None:
-            ev[0].record(stream)
-        s2l.s2l_kv_append(cache, batch, k_new, v_new, stream)
-        if ev is not None:
-            ev[1].record(stream)
-        plan = s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, stream)
-        if ev is not None:
-            ev[2].record(stream)
-        s2l.s2l_attn_main(cache, batch, q, HQ, scale, out, lse, plan, ws, stream)
-        if ev is not None:
-            ev[3].record(stream)
-        s2l.s2l_split_reduce(batch, HQ, out, lse, plan, ws, stream)
-        if ev is not None:
-            ev[4].record(stream)
-        return plan
+    # One step for layer copy l, in stream order: append, plan, attention, split merge.  (A
+    # plan on a forked stream beside the append measured slower inside a graph: the
+    # cross-stream dependencies cost more than the overlap saves.)
+    plan_box = {}
 
-    with torch.cuda.stream(stream):
-        for i in range(args.warmup):
-            plan = step(i)
+    def enqueue_step(l):
+        s2l.s2l_kv_append(caches[l], batch, k_new, v_new, main_stream)
+        plan_box["plan"] = s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, main_stream)
+        s2l.s2l_attn_main(caches[l], batch, q, HQ, scale, out, lse, plan_box["plan"], ws, main_stream)
+        s2l.s2l_split_reduce(batch, HQ, out, lse, plan_box["plan"], ws, main_stream)
+
+    # Every launch is captured once into HIP graphs and replayed, so that the timed regions
+    # measure the GPU, not the host's launch rate.
+    def capture(fn):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(main_stream):
+            with torch.cuda.graph(g, stream=main_stream):
+                fn()
+        return g
+
+    with torch.cuda.stream(main_stream):
+        enqueue_step(0)          # eager run: the plan exists before any single-kernel graph
+    torch.cuda.synchronize()
+    plan = plan_box["plan"]
+    # the warm-up steps and the K timed steps, one graph each (steps rotate over the layer copies)
+    warm_graph = capture(lambda: [enqueue_step(i % L) for i in range(args.warmup)]) if args.warmup else None
+    timed_graph = capture(lambda: [enqueue_step((args.warmup + i) % L) for i in range(args.steps)])
+    kernel_graphs = {
+        "append": capture(lambda: [s2l.s2l_kv_append(caches[l], batch, k_new, v_new, main_stream) for l in range(L)]),
+        "plan": capture(lambda: [s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, main_stream) for _ in range(L)]),
+        "attn_main": capture(lambda: [s2l.s2l_attn_main(caches[l], batch, q, HQ, scale, out, lse, plan, ws,
+                                                        main_stream) for l in range(L)]),
+        "split_reduce": capture(lambda: [s2l.s2l_split_reduce(batch, HQ, out, lse, plan, ws, main_stream)
+                                         for _ in range(L)]),
+    }
     torch.cuda.synchronize()
 
-    # timed region 1: the K steps back to back (whole-step throughput)
+    if warm_graph is not None:
+        with torch.cuda.stream(main_stream):
+            warm_graph.replay()
+    torch.cuda.synchronize()
+
+    # timed region 1: K steps back to back (whole-step throughput)
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     w0 = time.perf_counter()
-    t_start.record(stream)
-    for i in range(args.steps):
-        plan = step(args.warmup + i)
-    t_end.record(stream)
+    with torch.cuda.stream(main_stream):
+        t_start.record(main_stream)
+        timed_graph.replay()
+        t_end.record(main_stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
 
-    # timed region 2: the same K steps with events between the kernels (per-kernel times)
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for i in range(args.steps):
-        step(args.warmup + args.steps + i, evs[i])
-    torch.cuda.synchronize()
-    parts = np.array([[e[k].elapsed_time(e[k + 1]) for k in range(4)] for e in evs])  # ms
-    append_ms, plan_ms, main_ms, reduce_ms = [float(np.mean(parts[:, k])) for k in range(4)]
-    main_p10, main_p90 = float(np.percentile(parts[:, 2], 10)), float(np.percentile(parts[:, 2], 90))
+    # timed region 2: each kernel alone, L launches back to back per replay (average launch
+    # duration, HIP events on the stream the kernels run on)
+    per_kernel = {}
+    reps = max(1, args.steps // L + 1)
+    with torch.cuda.stream(main_stream):
+        for name, g in kernel_graphs.items():
+            g.replay()
+            times = []
+            for _ in range(reps):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(main_stream)
+                g.replay()
+                b.record(main_stream)
+                times.append((a, b))
+            torch.cuda.synchronize()
+            per_kernel[name] = [x.elapsed_time(y) / L for x, y in times]
+    main_ms = float(np.mean(per_kernel["attn_main"]))
+    step_breakdown = {k: round(float(np.mean(v)) * 1e3, 2) for k, v in per_kernel.items()}
+    # the step's outputs come from the graphs: check that the last replay left finite values
+    assert torch.isfinite(out.float()).all(), "non-finite attention output"
 
     flops = workloads.attn_flops([P], [C], HQ)
     value = flops / (ms_per_step * 1e-3) / 1e12
@@ -225,11 +258,11 @@ def main():
                    "prefix": P, "chunk": C, "num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": 128},
         "us_per_chunk": round(ms_per_step * 1e3, 2),
         "pct_mfma_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
-        "step_breakdown_us": {"append": round(append_ms * 1e3, 2), "plan": round(plan_ms * 1e3, 2),
-                              "attn_main": round(main_ms * 1e3, 2), "split_reduce": round(reduce_ms * 1e3, 2),
-                              "attn_main_p10": round(main_p10 * 1e3, 2), "attn_main_p90": round(main_p90 * 1e3, 2)},
+        "step_breakdown_us": step_breakdown,
+        "timing": "one HIP graph of the K steps, replayed once; per-kernel times are averages over "
+                  "graphs of back-to-back launches of that kernel",
         "plan": {"work_items": plan.num_items, "split_requests": plan.num_split_reqs,
-                 "split_keys": plan.split_keys, "tile_cols": plan.tile_cols},
+                 "split_keys": plan.split_keys, "tile_cols": plan.tile_cols, "key_halves": plan.key_halves},
         "wall_s_timed_region": round(wall, 4),
         "roofline": {"bound": "mfma", "kernel": "attn_main_kernel", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),

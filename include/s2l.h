@@ -44,7 +44,7 @@
 extern "C" {
 #endif
 
-#define S2L_ABI_VERSION 1
+#define S2L_ABI_VERSION 2
 #define S2L_HEAD_DIM 128
 #define S2L_PAGE_SIZE 16
 
@@ -103,11 +103,18 @@ typedef struct s2l_batch {
 
 /* Tunables of the work partitioner; pass NULL for the defaults. */
 typedef struct s2l_plan_opts {
-  int32_t target_items;    /* work items wanted before prefixes are split; 0 = automatic    */
+  int32_t target_items;    /* work items wanted before prefixes are split; 0 = the number   */
+                           /* of workgroups the GPU holds at once (CUs x 1 or x 2)          */
   int32_t min_split_keys;  /* smallest key range of a split piece; 0 = 512 (rounded to 64) */
   int32_t max_splits;      /* most pieces per request; 0 = 16 (at most 64)                  */
   int32_t tile_cols;       /* query columns (tokens x heads of one kv head) per work item:  */
-                           /* 128 (4-wave workgroups) or 256 (8 waves); 0 = automatic      */
+                           /* 128 or 256; 0 = automatic: 256 unless such tiles would be     */
+                           /* less than half full on average (mostly decode-like rows)      */
+  int32_t key_halves;      /* wave groups per work item, each taking half of its key range: */
+                           /* 1 (a 4-wave workgroup per 128 columns, two per CU; 8 waves,   */
+                           /* one per CU, for 256) or 2 (128 columns only: an 8-wave        */
+                           /* workgroup whose two groups merge their halves through LDS,    */
+                           /* one per CU); 0 = automatic: 2 for 128 columns, else 1         */
 } s2l_plan_opts;
 
 /* What a plan contains, returned to the host by s2l_attn_plan. */
@@ -121,6 +128,9 @@ typedef struct s2l_plan_info {
   int64_t total_tokens;    /* T                                                             */
   int64_t workspace_bytes; /* bytes of workspace this plan uses                            */
   int32_t tile_cols;       /* query columns per work item (128 or 256)                     */
+  int32_t num_tiles;       /* query tiles (a split tile has one item per key-range piece)   */
+  int64_t part_floats;     /* fp32 words of split partials in the workspace                 */
+  int32_t key_halves;      /* wave groups per work item (1 or 2)                            */
   int32_t reserved;
 } s2l_plan_info;
 
@@ -162,11 +172,14 @@ s2l_status s2l_attn_workspace_bytes(const s2l_batch* batch, int32_t num_q_heads,
 
 /*
  * Build the varlen work partition for one step and store it in the workspace (a small
- * kernel on `stream`); reuse it for every layer of the step.  Each request's chunk is cut
- * into query tiles of tile_cols / G tokens x G heads per kv head.  When the batch has fewer than
- * target_items tiles, each request's key range 0 .. P_r + i_end is split into up to
- * max_splits pieces of >= min_split_keys keys, so that long prefixes spread over more
- * workgroups (their partial results are merged by s2l_split_reduce).
+ * kernel on `stream`: per-request arrays and one 64-byte record per work item); reuse it
+ * for every layer of the step.  Each request's chunk is cut into query tiles of
+ * tile_cols / G tokens x G heads per kv head.  When the batch has fewer than target_items
+ * tiles, each request's key range 0 .. P_r + i_end is split into up to max_splits pieces of
+ * >= min_split_keys keys (never more items than target_items in total), so that long
+ * prefixes spread over more workgroups (their partial results are merged by
+ * s2l_split_reduce).  With key_halves = 2 a work item's own range is
+ * further halved between two wave groups of its workgroup, merged in LDS.
  *   workspace : device, ws_bytes >= s2l_attn_workspace_bytes(...).
  *   info      : HOST out, describes the plan; pass it to the attention calls.
  */
@@ -184,12 +197,13 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
  * K_r/V_r are read from the pages after the step's append (the chunk's own keys included;
  * for an fp8 cache these are its quantised values decode(code) * scale).  Precision: the
  * weights e^{s_j} / sum are applied as bf16 values normalised by their own sum, so out is
- * within about 2^-7 sum_j w_j |V_j - out| + 2^-8 |out| of the exact result; lse uses fp32
- * sums.
+ * within about 2^-7 sum_j w_j |V_j - out| + 2^-8 |out| of the exact result; lse is the
+ * log of the sum of those bf16 weights (within about 2^-8 of the exact value).
  *   q   : device bf16 [T][Hq][128] (post-RoPE).     out : device bf16 [T][Hq][128].
  *   lse : device fp32 [T][Hq] or NULL.               softmax_scale > 0 (e.g. 1/sqrt(128)).
  *   plan: the s2l_plan_info returned by s2l_attn_plan for this batch and head counts.
- * Equivalent to s2l_attn_main followed by s2l_split_reduce.
+ * Equivalent to s2l_attn_main followed by s2l_split_reduce (which enqueues nothing when
+ * no request is split).  Calls on one workspace must not overlap.
  */
 s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* batch,
                                   const void* q, int32_t num_q_heads, float softmax_scale,
@@ -199,8 +213,7 @@ s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* ba
 /*
  * The main attention kernel alone (online softmax over the work items of the plan).
  * Unsplit requests get their final out/lse; split requests get fp32 partials (unnormalised
- * output, then reference max and the two running sums) in the workspace, merged by
- * s2l_split_reduce.
+ * output, then reference max and running sum) in the workspace, merged by s2l_split_reduce.
  */
 s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch,
                          const void* q, int32_t num_q_heads, float softmax_scale,
@@ -210,7 +223,8 @@ s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch,
 /*
  * Log-sum-exp merge of split partials (online-softmax merge): for each row and head of a
  * split request, m* = max_s m_s, l* = sum_s l_s 2^(m_s - m*), out = sum_s acc_s 2^(m_s - m*) / l*
- * (bf16), lse = ln(2) (m* + log2 l*).  Enqueues nothing when the plan has no split request.
+ * (bf16), lse = ln(2) (m* + log2 l*) (m in the log2 domain).  Enqueues nothing when the
+ * plan has no split request.
  */
 s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* out, float* lse,
                             const s2l_plan_info* plan, const void* workspace, size_t ws_bytes,

@@ -122,9 +122,9 @@ class Batch:
             chunk_lens_host=self.chunk_host.ctypes.data_as(_lib.P_i32))
 
 
-def plan_opts(target_items=0, min_split_keys=0, max_splits=0, tile_cols=0):
+def plan_opts(target_items=0, min_split_keys=0, max_splits=0, tile_cols=0, key_halves=0):
     return s2l_plan_opts(target_items=target_items, min_split_keys=min_split_keys,
-                         max_splits=max_splits, tile_cols=tile_cols)
+                         max_splits=max_splits, tile_cols=tile_cols, key_halves=key_halves)
 
 
 def _opts_ptr(opts):

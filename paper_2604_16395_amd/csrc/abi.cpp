@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -37,24 +38,36 @@ s2l_status hip_fail(const char* what, hipError_t e) {
 }
 
 struct Resolved {
-  int32_t target_items, min_split_keys, max_splits, tile_cols;
+  int32_t target_items, min_split_keys, max_splits, tile_cols, key_halves;
 };
 
-// Automatic tile width: 256 columns halve the LDS traffic per MFMA when the batch has
-// enough query columns to keep every CU busy with such tiles; else 128.
+// Automatic tile width: 256-column tiles (8-wave workgroups sharing each K/V tile, with a
+// four-stage copy ring; the fastest layout measured on the 8K-prefix, 512-token step)
+// unless they would be less than half full on average, as in batches of mostly decode-like
+// rows (C * G well below 256 columns per request and kv head); then 128.
 int32_t auto_tile_cols(int32_t R, const int32_t* C, int32_t hq, int32_t hkv) {
-  (void)R; (void)C; (void)hq; (void)hkv;
-  return s2l::kMinTileCols;
+  const int64_t g = hq / hkv;
+  int64_t used = 0, alloc = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    const int64_t cols = (int64_t)C[r] * g;
+    used += cols;
+    alloc += s2l::ceil_div64(cols, s2l::kMaxTileCols) * s2l::kMaxTileCols;
+  }
+  return 2 * used >= alloc ? s2l::kMaxTileCols : s2l::kMinTileCols;
 }
 
 s2l_status resolve_opts(const s2l_plan_opts* o, bool need_cus, int32_t num_cus, int32_t R, const int32_t* C,
                         int32_t hq, int32_t hkv, Resolved* r) {
   int32_t t = o ? o->target_items : 0, m = o ? o->min_split_keys : 0, x = o ? o->max_splits : 0;
-  int32_t tc = o ? o->tile_cols : 0;
+  int32_t tc = o ? o->tile_cols : 0, kh = o ? o->key_halves : 0;
   if (t < 0 || m < 0 || x < 0) return fail(S2L_EINVAL, "plan opts must be >= 0");
   if (tc != 0 && tc != s2l::kMinTileCols && tc != s2l::kMaxTileCols)
     return fail(S2L_ENOTSUP, "tile_cols %d unsupported (0, 128 or 256)", tc);
+  if (kh < 0 || kh > 2) return fail(S2L_ENOTSUP, "key_halves %d unsupported (0, 1 or 2)", kh);
   r->tile_cols = tc != 0 ? tc : auto_tile_cols(R, C, hq, hkv);
+  if (r->tile_cols == s2l::kMaxTileCols && kh == 2)
+    return fail(S2L_ENOTSUP, "key_halves 2 needs 128-column tiles");
+  r->key_halves = kh != 0 ? kh : (r->tile_cols == s2l::kMaxTileCols ? 1 : 2);
   if (t == 0) {
     if (num_cus <= 0 && need_cus) {
       int dev = 0, n = 0;
@@ -64,7 +77,7 @@ s2l_status resolve_opts(const s2l_plan_opts* o, bool need_cus, int32_t num_cus, 
       num_cus = n;
     }
     if (num_cus <= 0) return fail(S2L_EINVAL, "num_cus must be > 0 when target_items is 0");
-    t = s2l::kDefaultItemsPerCu * num_cus;
+    t = s2l::items_per_cu(r->tile_cols, r->key_halves) * num_cus;
   }
   r->target_items = t;
   r->min_split_keys = (int32_t)s2l::align_up(m > 0 ? m : s2l::kDefaultMinSplitKeys, s2l::kKvTile);
@@ -139,18 +152,48 @@ s2l::KvLaunch kv_launch(const s2l_kv_cache* c, const s2l_batch* b) {
   return a;
 }
 
-// Host mirror of the device plan kernel (same rules, same order).
+// Items of the batch when every request is cut into pieces of at most split_keys keys.
+int64_t items_for(int32_t R, const int32_t* P, const int32_t* C, int32_t hkv, int32_t tq, int32_t split_keys,
+                  int32_t max_splits) {
+  int64_t n = 0;
+  for (int32_t r = 0; r < R; ++r)
+    n += (int64_t)hkv * s2l::num_qtiles(C[r], tq) * s2l::req_splits(P[r], C[r], split_keys, max_splits);
+  return n;
+}
+
+// Piece length of the batch: 0 (no split) when the batch already has at least target_items
+// query tiles; else the shortest multiple of 64 keys (at least min_split_keys) for which
+// cutting every request into ceil((P + C) / length) pieces (at most max_splits) gives no
+// more than target_items items, so that one round of workgroups covers the launch and the
+// longest item is as short as that allows.  Item counts fall as the length grows, so the
+// shortest such length is found by bisection.
+int32_t choose_split_keys(int32_t R, const int32_t* P, const int32_t* C, int32_t hkv, int32_t tq,
+                          const Resolved& o) {
+  int64_t tiles = 0, longest = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    tiles += (int64_t)hkv * s2l::num_qtiles(C[r], tq);
+    if (C[r] > 0 && (int64_t)P[r] + C[r] > longest) longest = (int64_t)P[r] + C[r];
+  }
+  if (tiles == 0 || tiles >= o.target_items) return 0;
+  const int64_t lo_keys = s2l::align_up(o.min_split_keys, s2l::kKvTile);
+  int64_t lo = lo_keys / s2l::kKvTile, hi = std::max(lo, s2l::ceil_div64(longest, s2l::kKvTile));
+  if (items_for(R, P, C, hkv, tq, (int32_t)(lo * s2l::kKvTile), o.max_splits) <= o.target_items) return (int32_t)(lo * s2l::kKvTile);
+  while (hi - lo > 1) {   // items(lo) > target >= items(hi); hi keys give one piece per tile
+    const int64_t mid = (lo + hi) / 2;
+    if (items_for(R, P, C, hkv, tq, (int32_t)(mid * s2l::kKvTile), o.max_splits) <= o.target_items) hi = mid;
+    else lo = mid;
+  }
+  return (int32_t)(hi * s2l::kKvTile);
+}
+
+// Host plan: the partition the device plan kernel stores (same rules, same order).
 void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_t hkv, const Resolved& o,
                s2l_plan_info* info, int32_t* items, int64_t cap) {
   const int32_t g = hq / hkv, tq = s2l::tile_tokens(g, o.tile_cols);
-  int64_t base = 0, work = 0, tokens = 0;
-  for (int32_t r = 0; r < R; ++r) {
-    base += (int64_t)s2l::num_qtiles(C[r], tq) * hkv;
-    work += s2l::req_work(P[r], C[r], tq) * hkv;
-    tokens += C[r];
-  }
-  const int32_t split_keys = s2l::split_keys_for(base, work, o.target_items, o.min_split_keys);
-  int64_t n_items = 0, part = 0;
+  int64_t tokens = 0;
+  for (int32_t r = 0; r < R; ++r) tokens += C[r];
+  const int32_t split_keys = choose_split_keys(R, P, C, hkv, tq, o);
+  int64_t n_items = 0, part = 0, n_tiles = 0;
   int32_t n_split = 0;
   for (int32_t r = 0; r < R; ++r) {
     const int32_t ns = s2l::req_splits(P[r], C[r], split_keys, o.max_splits);
@@ -170,6 +213,7 @@ void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_
           }
     }
     n_items += (int64_t)hkv * nqt * ns;
+    n_tiles += (int64_t)hkv * nqt;
     part += s2l::req_part_floats(ns, C[r], hq);
     n_split += ns > 1 ? 1 : 0;
   }
@@ -180,9 +224,21 @@ void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_
   info->num_kv_heads = hkv;
   info->num_reqs = R;
   info->total_tokens = tokens;
-  info->workspace_bytes = s2l::workspace_bytes_for(R, part);
+  info->workspace_bytes = s2l::plan_layout(R, n_items, n_tiles, part).end;
   info->tile_cols = o.tile_cols;
+  info->num_tiles = (int32_t)n_tiles;
+  info->part_floats = part;
+  info->key_halves = o.key_halves;
   info->reserved = 0;
+}
+
+s2l::PlanDims plan_dims(const s2l_plan_info* p) {
+  s2l::PlanDims d;
+  d.num_reqs = p->num_reqs;
+  d.num_items = p->num_items;
+  d.num_tiles = p->num_tiles;
+  d.part_floats = p->part_floats;
+  return d;
 }
 
 s2l_status check_plan(const s2l_plan_info* plan, const s2l_batch* b, int32_t hq, int32_t hkv, int64_t T,
@@ -193,6 +249,12 @@ s2l_status check_plan(const s2l_plan_info* plan, const s2l_batch* b, int32_t hq,
     return fail(S2L_EINVAL, "plan was made for another batch or head count");
   if (plan->tile_cols != s2l::kMinTileCols && plan->tile_cols != s2l::kMaxTileCols)
     return fail(S2L_EINVAL, "plan info has an invalid tile width %d", plan->tile_cols);
+  if (plan->key_halves != 1 && (plan->key_halves != 2 || plan->tile_cols != s2l::kMinTileCols))
+    return fail(S2L_EINVAL, "plan info has an invalid key_halves %d", plan->key_halves);
+  if (plan->num_items < 0 || plan->num_tiles < 0 || plan->part_floats < 0 ||
+      s2l::plan_layout(plan->num_reqs, plan->num_items, plan->num_tiles, plan->part_floats).end !=
+          plan->workspace_bytes)
+    return fail(S2L_EINVAL, "plan info is inconsistent (not as returned by s2l_attn_plan)");
   if (!ws) return fail(S2L_EWORKSPACE, "workspace is NULL");
   if ((int64_t)ws_bytes < plan->workspace_bytes)
     return fail(S2L_EWORKSPACE, "workspace %zu bytes < %lld needed", ws_bytes, (long long)plan->workspace_bytes);
@@ -211,6 +273,29 @@ s2l_status attn_common(const s2l_kv_cache* cache, const s2l_batch* batch, const 
   return check_plan(plan, batch, hq, cache->num_kv_heads, *T, ws, ws_bytes);
 }
 
+s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q, int32_t num_q_heads,
+                       float softmax_scale, void* out, float* lse, const s2l_plan_info* plan, void* workspace,
+                       size_t ws_bytes, void* stream) {
+  int64_t T = 0;
+  s2l_status st = attn_common(cache, batch, q, num_q_heads, softmax_scale, out, plan, workspace, ws_bytes, &T);
+  if (st != S2L_OK) return st;
+  s2l::AttnLaunch a;
+  a.kv = kv_launch(cache, batch);
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.hq = num_q_heads;
+  a.softmax_scale = softmax_scale;
+  a.workspace = workspace;
+  a.dims = plan_dims(plan);
+  a.tile_cols = plan->tile_cols;
+  a.key_halves = plan->key_halves;
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("attn_main launch", e);
+  return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -226,6 +311,8 @@ s2l_status s2l_kv_append(const s2l_kv_cache* cache, const s2l_batch* batch, cons
   if ((st = check_cache(cache, batch)) != S2L_OK) return st;
   if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
   if (T > 0 && (!k_new || !v_new)) return fail(S2L_EINVAL, "k_new/v_new is NULL");
+  if (batch->num_reqs > 65535 || cache->num_kv_heads > 65535)
+    return fail(S2L_ENOTSUP, "kv_append supports at most 65535 requests and kv heads");
   int32_t max_touched = 0;
   for (int32_t r = 0; r < batch->num_reqs; ++r) {
     const int32_t p = batch->prefix_lens_host[r], c = batch->chunk_lens_host[r];
@@ -309,14 +396,13 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
   a.num_reqs = batch->num_reqs;
   a.hq = num_q_heads;
   a.hkv = num_kv_heads;
-  a.target_items = o.target_items;
-  a.min_split_keys = o.min_split_keys;
+  a.split_keys = pi.split_keys;
   a.max_splits = o.max_splits;
   a.tile_cols = o.tile_cols;
   a.ws_bytes = (int64_t)ws_bytes;
   a.workspace = workspace;
   (void)hipGetLastError();
-  hipError_t e = s2l::launch_attn_plan(a, static_cast<hipStream_t>(stream));
+  hipError_t e = s2l::launch_attn_plan(a, plan_dims(&pi), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("attn_plan launch", e);
   *info = pi;
   return ok();
@@ -325,23 +411,7 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
 s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q, int32_t num_q_heads,
                          float softmax_scale, void* out, float* lse, const s2l_plan_info* plan, void* workspace,
                          size_t ws_bytes, void* stream) {
-  int64_t T = 0;
-  s2l_status st = attn_common(cache, batch, q, num_q_heads, softmax_scale, out, plan, workspace, ws_bytes, &T);
-  if (st != S2L_OK) return st;
-  s2l::AttnLaunch a;
-  a.kv = kv_launch(cache, batch);
-  a.q = q;
-  a.out = out;
-  a.lse = lse;
-  a.hq = num_q_heads;
-  a.softmax_scale = softmax_scale;
-  a.workspace = workspace;
-  a.num_items = plan->num_items;
-  a.tile_cols = plan->tile_cols;
-  (void)hipGetLastError();
-  hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return hip_fail("attn_main launch", e);
-  return ok();
+  return attn_launch(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes, stream);
 }
 
 s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* out, float* lse,
@@ -360,6 +430,7 @@ s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* o
   a.hq = num_q_heads;
   a.num_reqs = batch->num_reqs;
   a.total_tokens = T;
+  a.dims = plan_dims(plan);
   (void)hipGetLastError();
   hipError_t e = s2l::launch_split_reduce(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("split_reduce launch", e);
@@ -369,8 +440,8 @@ s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* o
 s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q,
                                   int32_t num_q_heads, float softmax_scale, void* out, float* lse,
                                   const s2l_plan_info* plan, void* workspace, size_t ws_bytes, void* stream) {
-  s2l_status st = s2l_attn_main(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes,
-                                stream);
+  s2l_status st = attn_launch(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes,
+                              stream);
   if (st != S2L_OK) return st;
   return s2l_split_reduce(batch, num_q_heads, out, lse, plan, workspace, ws_bytes, stream);
 }

@@ -1,6 +1,8 @@
 // Device plan kernel: computes the varlen work partition of one step from the device
-// length arrays (rules in plan_rules.h, identical to the host's) and stores it, with a
-// snapshot of the lengths, at the start of the caller's workspace.  One workgroup.
+// length arrays (rules in plan_rules.h, identical to the host's) and stores it at the start
+// of the caller's workspace: per-request arrays and one ItemRec per work item (so that an
+// attention workgroup finds all it needs in one scalar load).  One workgroup.  The piece
+// length comes from the host planner, which chose it from its copies of the lengths.
 #include "launch.h"
 #include "plan_rules.h"
 
@@ -10,93 +12,102 @@ namespace {
 
 constexpr int kPlanThreads = 256;
 constexpr int kPlanWaves = kPlanThreads / 64;
+constexpr int kLdsReqs = 1024;   // batches up to this size keep their per-request values in LDS
 
-// Block-wide exclusive scan of three int64 values; returns the block totals in tot[].
-__device__ void block_scan3(int64_t v[3], int64_t excl[3], int64_t tot[3], int64_t (*sh)[kPlanWaves]) {
+// Block-wide exclusive scan of N int64 values; returns the block totals in tot[].
+template <int N>
+__device__ void block_scan(const int64_t (&v)[N], int64_t (&excl)[N], int64_t (&tot)[N],
+                           int64_t (*sh)[kPlanWaves]) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int64_t x[3] = {v[0], v[1], v[2]};
+  int64_t x[N];
+  for (int k = 0; k < N; ++k) x[k] = v[k];
   for (int o = 1; o < 64; o <<= 1) {
-    for (int k = 0; k < 3; ++k) {
-      int64_t y = __shfl_up(x[k], o);
+    for (int k = 0; k < N; ++k) {
+      const int64_t y = __shfl_up(x[k], o);
       if (lane >= o) x[k] += y;
     }
   }
   if (lane == 63)
-    for (int k = 0; k < 3; ++k) sh[k][w] = x[k];
+    for (int k = 0; k < N; ++k) sh[k][w] = x[k];
   __syncthreads();
-  if (threadIdx.x == 0) {
-    int64_t run[3] = {0, 0, 0};
-    for (int i = 0; i < kPlanWaves; ++i)
-      for (int k = 0; k < 3; ++k) {
-        int64_t t = sh[k][i];
-        sh[k][i] = run[k];
-        run[k] += t;
-      }
-    for (int k = 0; k < 3; ++k) tot[k] = run[k];
+  for (int k = 0; k < N; ++k) {
+    int64_t before = 0, all = 0;
+    for (int i = 0; i < kPlanWaves; ++i) {
+      before += i < w ? sh[k][i] : 0;
+      all += sh[k][i];
+    }
+    excl[k] = before + x[k] - v[k];
+    tot[k] = all;
   }
-  __syncthreads();
-  for (int k = 0; k < 3; ++k) excl[k] = sh[k][w] + x[k] - v[k];
 }
 
+// Largest r with a[r] <= x, for a non-decreasing a[0..n] with a[0] <= x < a[n].
+template <typename A>
+__device__ inline int upper_index(const A& a, int n, int x) {
+  int lo = 0, hi = n;
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (a[mid] <= x) lo = mid; else hi = mid;
+  }
+  return lo;
+}
+
+// One pass over the requests (a contiguous segment per thread): pieces per request from the
+// host's piece length, then a block scan of items, partial floats, tiles, split requests
+// and tokens gives every offset and total.
 __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, PlanPtrs pp) {
-  __shared__ int64_t sh[3][kPlanWaves];
-  __shared__ int64_t tot[3];
+  __shared__ int64_t sh[5][kPlanWaves];
+  __shared__ int32_t s_item_off[kLdsReqs + 1];
+  __shared__ int32_t s_tile_off[kLdsReqs], s_ns[kLdsReqs], s_p[kLdsReqs], s_c[kLdsReqs], s_cu[kLdsReqs];
+  __shared__ int64_t s_part[kLdsReqs];
   const int R = a.num_reqs;
   const int G = a.hq / a.hkv;
   const int tq = tile_tokens(G, a.tile_cols);
-  int32_t* item_off = pp.item_off;
-  int32_t* nqt_a = pp.nqt;
-  int32_t* ns_a = pp.ns;
-  int32_t* p_a = pp.p;
-  int32_t* c_a = pp.c;
-  int32_t* cu_a = pp.cu;
-  int64_t* po_a = pp.part_off;
+  const int split_keys = a.split_keys;
 
-  // pass 1: tiles and keys of the whole batch
   const int seg = (R + kPlanThreads - 1) / kPlanThreads;
   const int r0 = threadIdx.x * seg, r1 = min(R, r0 + seg);
-  int64_t v[3] = {0, 0, 0}, excl[3];
-  for (int r = r0; r < r1; ++r) {
-    const int P = a.prefix_lens[r], C = a.chunk_lens[r];
-    v[0] += (int64_t)num_qtiles(C, tq) * a.hkv;
-    v[1] += req_work(P, C, tq) * a.hkv;
-    v[2] += C;
-  }
-  block_scan3(v, excl, tot, sh);
-  const int64_t base_items = tot[0], total_work = tot[1], total_tokens = tot[2];
-  const int32_t split_keys = split_keys_for(base_items, total_work, a.target_items, a.min_split_keys);
-  __syncthreads();
-
-  // pass 2: per-request pieces, item offsets and partial offsets
-  v[0] = v[1] = v[2] = 0;
+  int64_t v[5] = {0, 0, 0, 0, 0}, excl[5], tot[5];
   for (int r = r0; r < r1; ++r) {
     const int P = a.prefix_lens[r], C = a.chunk_lens[r];
     const int ns = req_splits(P, C, split_keys, a.max_splits);
-    v[0] += (int64_t)a.hkv * num_qtiles(C, tq) * ns;
+    const int64_t tiles = (int64_t)a.hkv * num_qtiles(C, tq);
+    v[0] += tiles * ns;
     v[1] += req_part_floats(ns, C, a.hq);
-    v[2] += ns > 1 ? 1 : 0;
+    v[2] += tiles;
+    v[3] += ns > 1 ? 1 : 0;
+    v[4] += C;
   }
-  block_scan3(v, excl, tot, sh);
-  const int64_t num_items = tot[0], part_floats = tot[1], num_split = tot[2];
-  const bool fits = workspace_bytes_for(R, part_floats) <= a.ws_bytes && num_items < ((int64_t)1 << 31);
-  int64_t items = excl[0], part = excl[1];
+  block_scan<5>(v, excl, tot, sh);
+  const int64_t num_items = tot[0], part_floats = tot[1], num_tiles = tot[2];
+  const bool fits = num_items <= pp.cap_items && num_tiles <= pp.cap_tiles && part_floats <= pp.cap_part_floats;
+  int64_t items = excl[0], part = excl[1], tiles = excl[2];
   for (int r = r0; r < r1; ++r) {
     const int P = a.prefix_lens[r], C = a.chunk_lens[r];
     const int ns = req_splits(P, C, split_keys, a.max_splits);
     const int nqt = num_qtiles(C, tq);
-    item_off[r] = (int32_t)items;
-    nqt_a[r] = nqt;
-    ns_a[r] = ns;
-    p_a[r] = P;
-    c_a[r] = C;
-    cu_a[r] = a.cu_chunk[r];
-    po_a[r] = part;
+    pp.item_off[r] = (int32_t)items;
+    pp.ns[r] = ns;
+    pp.c[r] = C;
+    pp.cu[r] = a.cu_chunk[r];
+    pp.part_off[r] = part;
+    if (R <= kLdsReqs) {
+      s_item_off[r] = (int32_t)items;
+      s_tile_off[r] = (int32_t)tiles;
+      s_ns[r] = ns;
+      s_p[r] = P;
+      s_c[r] = C;
+      s_cu[r] = a.cu_chunk[r];
+      s_part[r] = part;
+    }
     items += (int64_t)a.hkv * nqt * ns;
     part += req_part_floats(ns, C, a.hq);
+    tiles += (int64_t)a.hkv * nqt;
   }
   if (threadIdx.x == 0) {
-    item_off[R] = (int32_t)num_items;
-    cu_a[R] = a.cu_chunk[R];
+    pp.item_off[R] = (int32_t)num_items;
+    pp.cu[R] = a.cu_chunk[R];
+    if (R <= kLdsReqs) s_item_off[R] = (int32_t)num_items;
     PlanHeader* h = pp.hdr;
     h->magic = kPlanMagic;
     h->num_reqs = R;
@@ -105,20 +116,56 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     h->g = G;
     h->tq = tq;
     h->num_items = fits ? (int32_t)num_items : 0;
-    h->num_split_reqs = (int32_t)num_split;
+    h->num_split_reqs = (int32_t)tot[3];
     h->split_keys = split_keys;
     h->status = fits ? 0 : 1;
     h->tile_cols = a.tile_cols;
-    h->pad1 = 0;
+    h->num_tiles = (int32_t)num_tiles;
     h->part_floats = part_floats;
-    h->total_tokens = total_tokens;
+    h->total_tokens = tot[4];
+  }
+  if (!fits) return;
+  __syncthreads();   // request arrays (global and LDS) complete
+
+  // one record per item; the request of item w is found by binary search over item offsets
+  for (int w = threadIdx.x; w < (int)num_items; w += kPlanThreads) {
+    int r, tile0, P, C, ns, row0, off;
+    int64_t part_off;
+    if (R <= kLdsReqs) {
+      r = upper_index(s_item_off, R, w);
+      tile0 = s_tile_off[r];
+      P = s_p[r], C = s_c[r], ns = s_ns[r], row0 = s_cu[r], off = s_item_off[r], part_off = s_part[r];
+    } else {
+      r = upper_index(pp.item_off, R, w);
+      tile0 = 0;
+      for (int k = 0; k < r; ++k) tile0 += a.hkv * num_qtiles(a.chunk_lens[k], tq);
+      P = a.prefix_lens[r], C = a.chunk_lens[r], ns = pp.ns[r], row0 = a.cu_chunk[r], off = pp.item_off[r];
+      part_off = pp.part_off[r];
+    }
+    const int nqt = num_qtiles(C, tq);
+    const Item it = decode_local(w - off, nqt, ns);
+    ItemRec rec;
+    rec.r = r;
+    rec.g = it.g;
+    rec.i0 = it.qt * tq;
+    rec.i1 = min(rec.i0 + tq, C);
+    piece_range(P + rec.i1, ns, it.s, &rec.lo, &rec.hi);
+    rec.s = it.s;
+    rec.ns = ns;
+    rec.p = P;
+    rec.c = C;
+    rec.row0 = row0;
+    rec.tile = tile0 + it.g * nqt + it.qt;
+    rec.part_off = part_off;
+    rec.pad0 = rec.pad1 = 0;
+    pp.items[w] = rec;
   }
 }
 
 }  // namespace
 
-hipError_t launch_attn_plan(const PlanLaunch& a, hipStream_t stream) {
-  attn_plan_kernel<<<1, kPlanThreads, 0, stream>>>(a, plan_ptrs(a.workspace, a.num_reqs));
+hipError_t launch_attn_plan(const PlanLaunch& a, const PlanDims& dims, hipStream_t stream) {
+  attn_plan_kernel<<<1, kPlanThreads, 0, stream>>>(a, plan_ptrs(a.workspace, dims));
   return hipGetLastError();
 }
 

@@ -4,16 +4,26 @@
 // num_computed_tokens as in Sec. 4.2): query i of a request's new chunk (absolute position
 // t = P + i) attends to keys 0..t of that request, read through its block table.
 //
-// One workgroup = kWaves waves (4 or 8) = one work item of the plan: kv head g, 32 kWaves
-// packed query columns (tq tokens x G heads, token-major) and a key range [lo, hi).
+// One workgroup = one work item of the plan: kv head g, 32 kColWaves packed query columns
+// (tq tokens x G heads, token-major) and a key range [lo, hi).  With kHalves = 2 the
+// workgroup has two groups of kColWaves waves on the same columns, each taking one half of
+// the key range (in whole 64-key tiles) with its own K/V ring; the second group hands its
+// (O, m, l) to the first through LDS at the end and the first merges them (the log-sum-exp
+// merge of the online softmax), so a key range is split in two without any partials in
+// memory.  The item's description is one 64-byte record written by the plan kernel (a
+// single scalar load).
 //
 // Data movement.  K and V tiles of 64 keys x 128 are staged in LDS, one key row of 256
 // bytes each, 16-byte chunks permuted per row (K: chunk c of row r at c ^ (r & 15); V: at
 // c ^ 4 (r & 3)) so that the MFMA operand reads below hit 64 distinct banks.  bf16 pages
-// are copied straight from HBM into LDS (buffer_load ... lds), each wave moving one page of
-// the tile; the buffer descriptor of a page ends at key `hi`, so keys past it arrive as
-// zeros.  E4M3 pages go through registers and are widened to bf16 on the way (exact).  K
-// is fetched one tile ahead of V; both are double buffered.
+// are copied straight from HBM into LDS (buffer_load ... lds), each wave moving its share of
+// one page of the tile; the buffer descriptor of a page ends at key `hi`, so keys past it
+// arrive as zeros.  The tiles rotate through a ring of kStages LDS stages (four for the
+// 8-wave bf16 kernel, which runs alone on its CU; two otherwise): K(t) and V(t) are fetched
+// kStages - 1 iterations ahead of their use and each wave waits only for the copies that the
+// next step reads (vmcnt(N), N > 0), so HBM latency hides behind several tiles of MFMA
+// work.  Page ids come from scalar loads of the block table one iteration ahead.  E4M3 pages
+// go through registers and are widened to bf16 on the way (exact), with a two-stage ring.
 //
 // Compute, per wave (32 query columns, one per lane pair), per 32-key sub-block b:
 //   * S^T(b) = K Q^T with v_mfma_f32_32x32x16_bf16: A = K rows from LDS, B = Q held in
@@ -26,13 +36,15 @@
 //     accumulated sum makes the result independent of m;
 //   * O^T += V^T P^T with the same MFMA: A = V^T read from the key-major V tile with the
 //     transposing LDS read (ds_read_b64_tr_b16), B = bf16 P straight from the registers.
+//     The row sum l adds up exactly these bf16 probabilities (v_dot2_f32_bf16), so O / l
+//     applies weights that are normalised exactly; the log-sum-exp is m + log2 l.
 // The sub-blocks are software pipelined: while the softmax of sub-block b runs on the
 // VALU, the MFMA unit computes S(b+1) and O += P(b-1) V(b-1); P(b-1) is checked for
 // overflow at the start of step b, before it enters O.  The causal mask is applied only to
 // sub-blocks that reach past the first query token's position.
 //
-// Unsplit items write bf16 O = acc / l (and LSE); split items write fp32 partials
-// (acc, m, l) that split_reduce merges (log-sum-exp merge of Sec. 2.1's softmax).
+// Unsplit items write bf16 O = acc / l (and LSE).  Split items write fp32 partials
+// (acc, m, l) that split_reduce_kernel merges (log-sum-exp merge of Sec. 2.1's softmax).
 #include "launch.h"
 #include "plan_rules.h"
 #include "s2l_device.h"
@@ -44,22 +56,9 @@ namespace {
 constexpr int kRowBytes = kHeadDim * 2;              // one bf16 key row in LDS
 constexpr int kTileBytes = kKvTile * kRowBytes;      // 16 KiB
 constexpr int kSubBytes = 32 * kRowBytes;            // one 32-key sub-block of a tile
-constexpr int kKBuf = 0;                             // K tiles at 0 and 16 KiB
-constexpr int kVBuf = 2 * kTileBytes;                // V tiles at 32 and 48 KiB
-constexpr int kLdsBytes = 4 * kTileBytes;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kOverflow = 18446744073709551616.0f;   // 2^64: largest probability kept
-
-// Largest r with a[r] <= x, for a non-decreasing a[0..n] with a[0] <= x < a[n].
-__device__ inline int upper_index(const int32_t* a, int n, int x) {
-  int lo = 0, hi = n;  // invariant: a[lo] <= x < a[hi]
-  while (hi - lo > 1) {
-    int mid = (lo + hi) >> 1;
-    if (a[mid] <= x) lo = mid; else hi = mid;
-  }
-  return lo;
-}
 
 // Raw buffer loads: a resource descriptor (base, size in bytes) in SGPRs plus a per-lane
 // byte offset.  Offsets at or past the size read as zero.
@@ -74,20 +73,10 @@ typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 __device__ inline int clamp16(int x) { return x < 0 ? 0 : (x > 16 ? 16 : x); }
 
-// Block-table entry `idx` of the request (0 past its last page: the descriptor of such a
-// page then has size 0 and nothing is read from it).  Every lane loads the same entry.
-// The index goes into the scalar offset: a load with a VGPR address would make every later
-// write of that VGPR wait for the load.
-__device__ inline int32_t table_entry(const int32_t* bt, int idx, int last_page) {
-  const int n = last_page + 1;
-  return (int32_t)__builtin_amdgcn_raw_buffer_load_b32(make_rsrc(bt, 4 * n), 0u,
-                                                       __builtin_amdgcn_readfirstlane(4 * idx), 0);
-}
-
 // LDS-direct copy: 64 lanes x 16 bytes from a raw buffer (descriptor words in SGPRs) to the
 // 1 KiB of LDS at byte address `lds`, lane l's bytes at lds + 16 l.  Issued as inline
 // assembly so that the compiler does not treat every later LDS read as waiting on it; the
-// caller waits for vmcnt(0) and synchronises before the destination is read.
+// caller waits for the copy's vmcnt and synchronises before the destination is read.
 typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
 __device__ inline i32x4 sgpr_rsrc(const void* base, int32_t bytes) {
   const uint64_t a = reinterpret_cast<uint64_t>(base);
@@ -99,6 +88,30 @@ __device__ inline void lds_dma_b128(const i32x4& rs, uint32_t voff, uint32_t lds
   __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                    :: "s"(lds), "v"(voff), "s"(rs) : "m0");
 }
+
+// Wait until at most N vector-memory operations of this wave are outstanding (the older
+// ones, issued first, are then complete); lgkm and exp counters are not waited for.
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+// Lane `lane` of v into an SGPR, ordered with the surrounding assembly (the copies whose
+// descriptor it feeds and the waits before it).  The nops cover the lane-select read of an
+// SGPR written by SALU and the SGPR written here being read by a later buffer load.
+__device__ inline int32_t readlane_ordered(int32_t v, int32_t lane) {
+  int32_t r;
+  __asm__ volatile("s_nop 4\n\tv_readlane_b32 %0, %1, %2\n\ts_nop 4" : "=s"(r) : "v"(v), "s"(lane));
+  return r;
+}
+// LDS-direct copy of one dword per lane (lane l's dword to lds + 4 l), as lds_dma_b128.
+__device__ inline void lds_dma_b32(const i32x4& rs, uint32_t voff, uint32_t lds) {
+  __asm__ volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                   :: "s"(lds), "v"(voff), "s"(rs) : "m0");
+}
+
+// Wait until this wave's LDS operations are complete (before a barrier that publishes them).
+__device__ inline void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(15 | (3 << 14) | (7 << 4)); }
 
 // Sub-block max of the 16 scores a lane holds, then over the lane pair (l, l ^ 32).  The
 // scores come straight from MFMAs: the max must be ordinary code (the compiler forms
@@ -117,48 +130,77 @@ template <bool kQK, bool kReads>
 __device__ inline void slot_schedule() {
   if constexpr (kQK) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);     // VALU
+    __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);     // VALU
     if constexpr (kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read (K)
   }
   __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-  __builtin_amdgcn_sched_group_barrier(0x002, kQK ? 3 : 7, 0);
+  __builtin_amdgcn_sched_group_barrier(0x002, kQK ? 3 : 6, 0);
   if constexpr (kReads) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // LDS reads (V)
 }
 
-template <bool kFp8, int kWaves>
-__global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
+// Weight 2^(m_s - m*) of a piece in the log-sum-exp merge (0 for an empty piece).
+__device__ inline float merge_weight(float m_s, float mstar) {
+  return m_s == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_s - mstar);
+}
+
+// LDS of one group of waves: a K/V ring of kStages 16 KiB tiles each (four stages for the
+// 8-column-wave bf16 kernel, which runs alone on its CU; two otherwise).
+template <bool kFp8, int kColWaves, int kHalves>
+struct Ring {
+  static constexpr int kStages = (!kFp8 && kColWaves == 8) ? 4 : 2;
+  static constexpr int kGroupBytes = 2 * kStages * kTileBytes;
+  static constexpr int kBytes = kHalves * kGroupBytes;
+};
+
+template <bool kFp8, int kColWaves, int kHalves>
+__global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)) void attn_main_kernel(
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out, float* __restrict__ lse,
     const void* __restrict__ kpool, const void* __restrict__ vpool, const float* __restrict__ kscale,
-    const float* __restrict__ vscale, const int32_t* __restrict__ block_tables, int32_t max_pages,
-    int32_t num_reqs, int32_t hq, int32_t hkv, float scale_log2, PlanPtrs pv) {
-  constexpr int kQuarters = kWaves / 4;              // waves sharing one page of a tile
+    const float* __restrict__ vscale, const int32_t* __restrict__ block_tables, int32_t max_pages, int32_t hq,
+    int32_t hkv, float scale_log2, PlanPtrs pv) {
+  using RingT = Ring<kFp8, kColWaves, kHalves>;
+  constexpr int kWaves = kColWaves * kHalves;
+  constexpr int kS = RingT::kStages;
+  static_assert(kHalves == 1 || kHalves == 2, "one or two key-range groups");
+  static_assert(kHalves == 1 || kColWaves * 32 * 128 * 4 + kColWaves * 64 * 8 <= RingT::kBytes,
+                "the second group's (O, m, l) fits in the LDS of the rings");
+  constexpr int kQuarters = kColWaves / 4;           // waves sharing one page of a tile
   constexpr int kRowsPerWave = 16 / kQuarters;       // key rows each wave moves per tile
   constexpr int kDma = kRowsPerWave / 4;             // bf16: 1 KiB LDS-direct loads per wave
   constexpr int kF8Loads = kRowsPerWave / 8;         // e4m3: 16-byte loads per lane
   constexpr int kRun = kFp8 ? 16 * 128 : 16 * 128 * 2;   // bytes of one (page, kv head)
   constexpr int kKeyBytes = kRun / 16;
-  __shared__ __attribute__((aligned(1024))) uint8_t smem[kLdsBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[RingT::kBytes];
+  __shared__ __attribute__((aligned(256))) int32_t s_pages[kWaves][2][64];   // next page windows
 
+  // the item (one scalar load) and the device plan's item count, fetched together
+  const int w_item = xcd_logical(blockIdx.x, gridDim.x);
+  const ItemRec it = pv.items[w_item];
   const int W = pv.hdr->num_items;
-  if ((int)blockIdx.x >= W) return;
-  const int w_item = xcd_logical(blockIdx.x, gridDim.x < (unsigned)W ? gridDim.x : W);
-  const int r = upper_index(pv.item_off, num_reqs, w_item);
-  const int nqt = pv.nqt[r], ns = pv.ns[r];
-  const Item it = decode_local(w_item - pv.item_off[r], nqt, ns);
-  const int P = pv.p[r], C = pv.c[r], row0 = pv.cu[r];
+  if (w_item >= W) return;   // the device plan did not fit this launch (nothing planned)
+  const int P = it.p, C = it.c, row0 = it.row0, ns = it.ns, g = it.g;
+  const int i0 = it.i0, i1 = it.i1;
   const int G = hq / hkv;
-  const int tq = tile_tokens(G, 32 * kWaves);
-  const int i0 = it.qt * tq;
-  const int i1 = min(i0 + tq, C);
-  int lo, hi;
-  piece_range(P + i1, ns, it.s, &lo, &hi);
-  const int g = it.g;
-  const int32_t* bt = block_tables + (int64_t)r * max_pages;
+  const int tq = tile_tokens(G, 32 * kColWaves);
+  const int32_t* bt = block_tables + (int64_t)it.r * max_pages;
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int grp = wave / kColWaves;                  // key-range group (0 or 1)
+  const int cw = wave % kColWaves;                   // column wave within the group
   const int n = lane & 31, half = lane >> 5;
-  const int col = wave * 32 + n;
+  const int col = cw * 32 + n;
+  // This group's key range: the item's [it.lo, it.hi) cut into two halves of whole tiles
+  // (the second may be a tile shorter, or empty); both groups step through nt0 tiles.
+  const int nt_all = it.hi > it.lo ? ceil_div(it.hi - it.lo, kKvTile) : 0;
+  const int nt0 = kHalves == 2 ? (nt_all + 1) >> 1 : nt_all;
+  const int lo = it.lo + grp * nt0 * kKvTile;
+  const int hi = kHalves == 2 && grp == 0 ? min(it.hi, lo + nt0 * kKvTile) : max(it.hi, lo);
+  // LDS offsets below are relative to the group's ring at grp_base (folded into the per-lane
+  // operand offsets and the copy destinations); K stages first, then V stages.
+  const int grp_base = grp * RingT::kGroupBytes;
+  constexpr int kKBase = 0;
+  constexpr int kVBase = kS * kTileBytes;
   const int tok = i0 + col / G;
   const int hq_col = g * G + col % G;
   const bool valid = col < tq * G && tok < i1;
@@ -186,7 +228,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
   // K (A of S^T = K Q^T), k-step ks, sub-block 0: row n, chunk 2 ks + half.
   uint32_t ka[8];
 #pragma unroll
-  for (int ks = 0; ks < 8; ++ks) ka[ks] = n * kRowBytes + ((((2 * ks + half) ^ (n & 15))) << 4);
+  for (int ks = 0; ks < 8; ++ks) ka[ks] = grp_base + n * kRowBytes + ((((2 * ks + half) ^ (n & 15))) << 4);
   // V^T (A of O^T += V^T P^T), d-block db, first 4-key set of k-step 0: within each group
   // of 16 lanes, lane j addresses key row (j >> 2) at column 32 db + 16 ((l >> 4) & 1) +
   // 4 (j & 3); the transposing read hands lane i the four keys of column base + i, so lane
@@ -198,12 +240,12 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
     const int row = 4 * half + (j >> 2);
 #pragma unroll
     for (int db = 0; db < 4; ++db)
-      va[db] = row * kRowBytes + ((4 * (db ^ ((j >> 2) & 3)) + 2 * b4 + ((j >> 1) & 1)) << 4) + 8 * (j & 1);
+      va[db] = grp_base + row * kRowBytes + ((4 * (db ^ ((j >> 2) & 3)) + 2 * b4 + ((j >> 1) & 1)) << 4) + 8 * (j & 1);
   }
 
-  // Tile loads: wave w moves rows [s0, s0 + kRowsPerWave) of page pw of each tile.
-  const int pw = wave / kQuarters;
-  const int s0 = (wave % kQuarters) * kRowsPerWave;
+  // Tile loads: column wave cw moves rows [s0, s0 + kRowsPerWave) of page pw of each tile.
+  const int pw = cw / kQuarters;
+  const int s0 = (cw % kQuarters) * kRowsPerWave;
   uint32_t kvo[kFp8 ? kF8Loads : kDma], vvo[kFp8 ? kF8Loads : kDma];
   if constexpr (!kFp8) {
     // LDS-direct load d writes tile rows 16 pw + s0 + 4d + (l >> 4), chunk l & 15: it
@@ -227,20 +269,42 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
   const char* vpb = static_cast<const char*>(vpool) + (int64_t)g * kRun;
   const int64_t page_stride = (int64_t)hkv * kRun;
 
-  // Page pg of the tile at key kb into the K or V buffer at `dst` (bf16: LDS-direct).
-  struct F8Stage {
-    u32x4 x[kF8Loads];
+  const int ntiles = nt0;                            // tile steps (the same in both groups)
+  const int last_page = hi > lo ? (hi - 1) >> 4 : (it.hi > it.lo ? (it.hi - 1) >> 4 : 0);
+  // Page ids.  Lane l of pg_win holds the physical page of this wave's page of tile
+  // win0 + l (block-table entry lo/16 + 4 (win0 + l) + pw, clamped to the item's last
+  // page, whose entry exists: a tile past the range is copied with a size-0 descriptor).
+  // The next 64-tile window is copied into this wave's LDS slot 64 tiles before it is
+  // needed, by an LDS-direct load that the per-iteration vmcnt waits cover (it is older than
+  // the copies they wait for), and read into pg_win when the window moves on.  Page ids
+  // never come from scalar loads inside the loop: those share lgkmcnt with the LDS reads,
+  // whose waits would then all be full waits.
+  const i32x4 bt_rs = sgpr_rsrc(bt, 4 * (last_page + 1));
+  auto win_offset = [&](int w0) -> uint32_t {
+    const int idx = (lo >> 4) + 4 * (w0 + lane) + pw;
+    return 4u * (uint32_t)(idx < last_page ? idx : last_page);
   };
-  auto dma_rows = [&](const char* base, int32_t pg, int kb, int dst, const uint32_t* vo, bool is_k) {
+  int32_t pg_win = bt[(win_offset(0) >> 2)];     // tracked load, waited for with the Q loads
+  int win0 = 0, win_slot = 0;
+  auto fetch_window = [&](int w0, int slot) {
+    lds_dma_b32(bt_rs, win_offset(w0),
+                __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void*)&s_pages[wave][slot][0]));
+  };
+  auto page_of = [&](int j) -> int32_t { return readlane_ordered(pg_win, j - win0); };
+
+  // Page pg of the tile at key kb into the buffer at LDS byte `dst` (bf16: LDS-direct).
+  auto dma_rows = [&](const char* base, int32_t pg, int kb, int dst, const uint32_t* vo) {
     const int bytes = __builtin_amdgcn_readfirstlane(clamp16(hi - (kb + 16 * pw)) * kKeyBytes);
     const i32x4 rs = sgpr_rsrc(base + (int64_t)pg * page_stride, bytes);
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)smem;
 #pragma unroll
     for (int d = 0; d < kDma; ++d) {
       const int row = 16 * pw + s0 + 4 * d;
-      lds_dma_b128(rs, vo[d], __builtin_amdgcn_readfirstlane(lds0 + dst + row * kRowBytes));
+      lds_dma_b128(rs, vo[d], __builtin_amdgcn_readfirstlane(lds0 + grp_base + dst + row * kRowBytes));
     }
-    (void)is_k;
+  };
+  struct F8Stage {
+    u32x4 x[kF8Loads];
   };
   auto f8_load = [&](F8Stage& st, const char* base, int32_t pg, int kb, const uint32_t* vo) {
     const int bytes = __builtin_amdgcn_readfirstlane(clamp16(hi - (kb + 16 * pw)) * kKeyBytes);
@@ -260,7 +324,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
       const u32x2 b = fp8x4_to_bf16x4(st.x[i][1]);
       const u32x2 c = fp8x4_to_bf16x4(st.x[i][2]);
       const u32x2 d = fp8x4_to_bf16x4(st.x[i][3]);
-      uint8_t* rp = smem + dst + row * kRowBytes;
+      uint8_t* rp = smem + grp_base + dst + row * kRowBytes;
       *reinterpret_cast<u32x4*>(rp + (((2 * f) ^ sw) << 4)) = u32x4{a[0], a[1], b[0], b[1]};
       *reinterpret_cast<u32x4*>(rp + (((2 * f + 1) ^ sw) << 4)) = u32x4{c[0], c[1], d[0], d[1]};
     }
@@ -269,13 +333,8 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
   f32x16 o[4];
 #pragma unroll
   for (int db = 0; db < 4; ++db) o[db] = f32x16{};
-  // Row sums per lane: b sums the bf16 probabilities exactly as P.V uses them (O is
-  // normalised by it), f sums them unrounded in fp32 (the log-sum-exp).
-  struct Sums {
-    float b, f;
-  };
   float m_run = 0.f;
-  Sums l_run = {0.f, 0.f};
+  float l_run = 0.f;   // sum of the bf16 probabilities exactly as P.V uses them
 
   // S(b+1) = K(b+1) Q^T from the sub-block at LDS byte `kofs`.
   auto qk = [&](int kofs) {
@@ -287,22 +346,6 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
     }
     return s;
   };
-  // O += P V over the sub-block whose V rows start at LDS byte `vofs`.
-  auto pv_acc = [&](const u32x4* p, int vofs) {
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      const bf16x8 pb = __builtin_bit_cast(bf16x8, p[k2]);
-#pragma unroll
-      for (int db = 0; db < 4; ++db) {
-        const uint8_t* base = smem + vofs + 16 * k2 * kRowBytes + va[db];
-        const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base));
-        const v4i16 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + 8 * kRowBytes));
-        const u32x2 ux = __builtin_bit_cast(u32x2, x), uy = __builtin_bit_cast(u32x2, y);
-        const bf16x8 a = __builtin_bit_cast(bf16x8, u32x4{ux[0], ux[1], uy[0], uy[1]});
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb, o[db], 0, 0, 0);
-      }
-    }
-  };
   // One A fragment of O^T += V^T P^T: keys 16 k2 + (4-key sets of this lane half), d-block db.
   auto read_v = [&](int vofs, int k2, int db) {
     const uint8_t* base = smem + vofs + 16 * k2 * kRowBytes + va[db];
@@ -310,6 +353,15 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
     const v4i16 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + 8 * kRowBytes));
     const u32x2 ux = __builtin_bit_cast(u32x2, x), uy = __builtin_bit_cast(u32x2, y);
     return __builtin_bit_cast(bf16x8, u32x4{ux[0], ux[1], uy[0], uy[1]});
+  };
+  // O += P V over the sub-block whose V rows start at LDS byte `vofs`.
+  auto pv_acc = [&](const u32x4* p, int vofs) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, p[k2]);
+#pragma unroll
+      for (int db = 0; db < 4; ++db) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(read_v(vofs, k2, db), pb, o[db], 0, 0, 0);
+    }
   };
   auto read_k = [&](int kofs, int ks) { return *reinterpret_cast<const bf16x8*>(smem + kofs + ka[ks]); };
   // Operands of a step's first two slots, read before its (branchy) softmax prologue.
@@ -330,7 +382,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
   // V^T P(b-1) (k2 = i / 4, db = i % 4) and the probabilities of score elements 2i, 2i+1
   // of sub-block b, while the operands of slot i + 2 are read from LDS.
   auto step_main = [&](const f32x16& s, const u32x4* pp, u32x4* po, int kofs, int vofs, const Pre& f,
-                       auto with_qk, Sums& lsum) {
+                       auto with_qk, float& lsum) {
     constexpr bool kQK = decltype(with_qk)::value;
     f32x16 sn = f32x16{};
     bf16x8 kf[10], vf[10];
@@ -338,7 +390,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
     kf[1] = f.k[1];
     vf[0] = f.v[0];
     vf[1] = f.v[1];
-    float l0 = 0.f, l1 = 0.f, f0 = 0.f, f1 = 0.f;
+    float l0 = 0.f, l1 = 0.f;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       if (i + 2 < 8) {
@@ -352,16 +404,11 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
       const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * i + 1], c_log2, -m_run));
       const uint32_t pk = pack_bf16x2(p0, p1);
       po[i >> 2][i & 3] = pk;
-      if (i & 1) {
-        l1 = sum_bf16x2(pk, l1);
-        f1 += p0 + p1;
-      } else {
-        l0 = sum_bf16x2(pk, l0);
-        f0 += p0 + p1;
-      }
+      if (i & 1) l1 = sum_bf16x2(pk, l1);
+      else l0 = sum_bf16x2(pk, l0);
     }
-    lsum = Sums{l0 + l1, f0 + f1};
-    __asm__ volatile("" ::"v"(po[0]), "v"(po[1]), "v"(lsum.b), "v"(lsum.f));   // produced here, not sunk
+    lsum = l0 + l1;
+    __asm__ volatile("" ::"v"(po[0]), "v"(po[1]), "v"(lsum));   // produced here, not sunk
     slot_schedule<kQK, true>();
     slot_schedule<kQK, true>();
     slot_schedule<kQK, true>();
@@ -372,19 +419,22 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
     slot_schedule<kQK, false>();
     return sn;
   };
-  // Causal mask of sub-block sb0 (element e of a lane's scores is key sb0 + 8 (e / 4) +
-  // 4 half + e % 4), applied only where the sub-block reaches past the first query token.
+  // Mask of sub-block sb0 (element e of a lane's scores is key sb0 + 8 (e / 4) + 4 half +
+  // e % 4): keys past the column's position (causal) or at or past the group's range end,
+  // applied only where the sub-block reaches past the first query token or the range end.
+  const int mask_from = min(P + i0, hi - 1);
+  const int key_lim = min(horizon, hi - 1);
   auto mask = [&](f32x16& s, int sb0) {
-    if (sb0 + 31 > P + i0) {
+    if (sb0 + 31 > mask_from) {
       __asm__ volatile("" ::);   // keep this a branch (not predicated into every sub-block)
-      const int lim = horizon - sb0 - 4 * half;
+      const int lim = key_lim - sb0 - 4 * half;
 #pragma unroll
       for (int e = 0; e < 16; ++e) s[e] = 8 * (e >> 2) + (e & 3) > lim ? -INFINITY : s[e];
     }
   };
-  // exp2(s c - m) -> bf16 pairs (k-slot order of the B operand) and both row sums.
-  auto probs = [&](const f32x16& s, u32x4* p, Sums& lsum) {
-    float l0 = 0.f, l1 = 0.f, f0 = 0.f, f1 = 0.f;
+  // exp2(s c - m) -> bf16 pairs (k-slot order of the B operand) and their row sum.
+  auto probs = [&](const f32x16& s, u32x4* p, float& lsum) {
+    float l0 = 0.f, l1 = 0.f;
 #pragma unroll
     for (int e = 0; e < 16; e += 4) {
       const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[e], c_log2, -m_run));
@@ -396,10 +446,8 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
       p[e >> 3][((e >> 1) & 3) + 1] = pk1;
       l0 = sum_bf16x2(pk0, l0);
       l1 = sum_bf16x2(pk1, l1);
-      f0 += p0 + p1;
-      f1 += p2 + p3;
     }
-    lsum = Sums{l0 + l1, f0 + f1};
+    lsum = l0 + l1;
   };
   // Settles the probabilities P of the previous sub-block (scores s, row sum lsum) before
   // they enter O.  They were computed against the running reference m; only when one of
@@ -407,99 +455,69 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
   // reference raised to that sub-block's exact max: O and l, which hold only earlier
   // sub-blocks, are rescaled and P is recomputed (rare branch).  Then the sum joins l.  The
   // reference of a column is shared by its lane pair, and so is the decision.
-  auto settle = [&](const f32x16& s, u32x4* p, Sums& lsum) {
-    if (__builtin_amdgcn_ballot_w64(lsum.f > kOverflow) != 0) {
+  auto settle = [&](const f32x16& s, u32x4* p, float& lsum) {
+    if (__builtin_amdgcn_ballot_w64(lsum > kOverflow) != 0) {
       __asm__ volatile("" ::);
-      const bool over = max_with_partner(lsum.f) > kOverflow;
+      const bool over = max_with_partner(lsum) > kOverflow;
       const float t = block_max(s) * c_log2;
       const float m_new = over ? t : m_run;
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
 #pragma unroll
       for (int db = 0; db < 4; ++db) o[db] *= alpha;
-      l_run.b *= alpha;
-      l_run.f *= alpha;
+      l_run *= alpha;
       m_run = m_new;
       probs(s, p, lsum);
     }
-    l_run.b += lsum.b;
-    l_run.f += lsum.f;
-  };
-
-  const int ntiles = hi > lo ? ceil_div(hi - lo, kKvTile) : 0;
-  const int last_page = hi > lo ? (hi - 1) >> 4 : 0;
-  const int P_i0 = P + i0;
-  (void)P_i0;
-
-  auto load_k = [&](int t, int32_t pg, int buf) {  // K of tile t into K buffer buf
-    if constexpr (!kFp8) dma_rows(kpb, pg, lo + t * kKvTile, kKBuf + buf * kTileBytes, kvo, true);
-  };
-  auto load_v = [&](int t, int32_t pg, int buf) {
-    if constexpr (!kFp8) dma_rows(vpb, pg, lo + t * kKvTile, kVBuf + buf * kTileBytes, vvo, false);
+    l_run += lsum;
   };
 
   f32x16 sp, sc;                 // scores of the previous and the current sub-block
   u32x4 pa[2], pb[2];
-  Sums lsum_p = {0.f, 0.f};      // row sums of the probabilities not yet settled
-  int32_t pg_next_v = 0;       // page (this wave's) of the tile whose V is loaded next
-  int32_t pid_v = 0;           // vector copy of a page-table entry loaded ahead
+  float lsum_p = 0.f;            // row sum of the probabilities not yet settled
+  int32_t pg_klast = 0;          // page of the last K tile whose copy was issued
+  int32_t pg_knext = 0;          // page of the next K tile (loaded one iteration ahead)
   F8Stage kst, vst;
 
-  if (ntiles > 0) {
-    const int e0 = table_entry(bt, (lo >> 4) + pw, last_page);
-    const int e1 = ntiles > 1 ? table_entry(bt, ((lo + kKvTile) >> 4) + pw, last_page) : 0;
-    if (ntiles > 2) pid_v = table_entry(bt, ((lo + 2 * kKvTile) >> 4) + pw, last_page);
-    __builtin_amdgcn_s_waitcnt(0);
-    const int32_t pg0 = __builtin_amdgcn_readfirstlane(e0);
-    const int32_t pg1 = __builtin_amdgcn_readfirstlane(e1);
+  // Moves the page window on when tile u leaves it (uniform, once per 64 tiles) and fetches
+  // the window after it into the other slot.  The new window's copy was issued 64 tiles
+  // earlier, before every copy the waits at the top of the last iterations covered, so it
+  // is in LDS.
+  auto advance_window = [&](int u) {
+    if (u - win0 == 64) {
+      pg_win = s_pages[wave][win_slot][lane];
+      win0 += 64;
+      win_slot ^= 1;
+      if (ntiles > win0 + 64 - kS - 2) fetch_window(win0 + 64, win_slot);
+    }
+  };
+
+  // Iteration t: copies V(t + kS - 1) and K(t + kS); sub-blocks 2t+1 and 2t+2 take the
+  // softmax, their successors S from K(t + 1), their predecessors O += P V from V(t).
+  // The ring stage of tile t is t % kS (a compile-time constant in each unrolled copy).
+  auto iteration = [&](int t, auto stage) {
+    constexpr int kJ = decltype(stage)::value;
+    const int kcur = kKBase + ((kJ + 1) % kS) * kTileBytes;   // K(t + 1)
+    const int vcur = kVBase + kJ * kTileBytes;                // V(t)
     if constexpr (!kFp8) {
-      load_k(0, pg0, 0);
-      load_v(0, pg0, 0);
-      if (ntiles > 1) load_k(1, pg1, 1);
+      // K(t + 1) and V(t) are this wave's copies issued before the last 2 kS - 4 groups of
+      // kDma; after the barrier every wave's share of them is in LDS, and every wave has
+      // finished iteration t - 1, whose stages the copies below overwrite.
+      wait_vmcnt<(2 * kS - 4) * kDma>();
+      __builtin_amdgcn_s_barrier();
+      dma_rows(vpb, pg_klast, lo + (t + kS - 1) * kKvTile, kVBase + ((kJ + kS - 1) % kS) * kTileBytes, vvo);
+      dma_rows(kpb, pg_knext, lo + (t + kS) * kKvTile, kKBase + kJ * kTileBytes, kvo);
+      pg_klast = pg_knext;
+      advance_window(t + kS + 1);
+      pg_knext = page_of(t + kS + 1);
     } else {
-      f8_load(kst, kpb, pg0, lo, kvo);
-      f8_load(vst, vpb, pg0, lo, vvo);
-      __builtin_amdgcn_s_waitcnt(0);
-      f8_store(kst, kKBuf, true);
-      f8_store(vst, kVBuf, false);
-      if (ntiles > 1) {
-        f8_load(kst, kpb, pg1, lo + kKvTile, kvo);
-        __builtin_amdgcn_s_waitcnt(0);
-        f8_store(kst, kKBuf + kTileBytes, true);
-      }
+      wait_lgkmcnt0();
+      __builtin_amdgcn_s_barrier();   // the stores of iteration t - 1 are visible
+      f8_load(vst, vpb, pg_klast, lo + (t + 1) * kKvTile, vvo);
+      f8_load(kst, kpb, pg_knext, lo + (t + 2) * kKvTile, kvo);
+      pg_klast = pg_knext;
+      advance_window(t + 3);
+      pg_knext = page_of(t + 3);
     }
-    pg_next_v = pg1;
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-
-    // Sub-block 0 sets the reference to its own max (a lane with no visible key there has
-    // none in the whole piece, as its visible keys form a prefix of the range).
-    sp = qk(kKBuf);
-    mask(sp, lo);
-    {
-      const float t = block_max(sp) * c_log2;
-      m_run = t == -INFINITY ? 0.f : t;
-    }
-    probs(sp, pa, lsum_p);
-    sc = qk(kKBuf + kSubBytes);
-    __syncthreads();   // K tile 0 is overwritten by the first iteration's loads
-  }
-
-  // Iteration t: loads K(t + 2), V(t + 1); sub-blocks 2t+1 and 2t+2 take the softmax, their
-  // successors S from K(t + 1), their predecessors O += P V from V(t).  kPar = t & 1.
-  auto iteration = [&](int t, auto par) {
-    constexpr int kPar = decltype(par)::value;
-    const int kcur = kKBuf + (kPar ^ 1) * kTileBytes;   // K(t + 1)
-    const int vcur = kVBuf + kPar * kTileBytes;         // V(t)
-    const int32_t pg_v = pg_next_v;
-    if (t + 2 < ntiles) {
-      const int32_t pg_k = __builtin_amdgcn_readfirstlane(pid_v);
-      if (t + 3 < ntiles) pid_v = table_entry(bt, ((lo + (t + 3) * kKvTile) >> 4) + pw, last_page);
-      if constexpr (!kFp8) load_k(t + 2, pg_k, kPar);
-      else f8_load(kst, kpb, pg_k, lo + (t + 2) * kKvTile, kvo);
-      pg_next_v = pg_k;
-    }
-    if constexpr (!kFp8) load_v(t + 1, pg_v, kPar ^ 1);
-    else f8_load(vst, vpb, pg_v, lo + (t + 1) * kKvTile, vvo);
 
     const int sb1 = lo + (2 * t + 1) * 32;
     constexpr std::true_type kWithQK{};
@@ -508,7 +526,7 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
       const Pre f = prefetch(kcur, vcur, kWithQK);
       settle(sp, pa, lsum_p);
       mask(sc, sb1);
-      Sums ls;
+      float ls;
       const f32x16 sn = step_main(sc, pa, pb, kcur, vcur, f, kWithQK, ls);
       sp = sc;
       sc = sn;
@@ -519,52 +537,153 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
       const Pre f = prefetch(kcur + kSubBytes, vcur + kSubBytes, kWithQK);
       settle(sp, pb, lsum_p);
       mask(sc, sb1 + 32);
-      Sums ls;
+      float ls;
       const f32x16 sn = step_main(sc, pb, pa, kcur + kSubBytes, vcur + kSubBytes, f, kWithQK, ls);
       sp = sc;
       sc = sn;
       lsum_p = ls;
     }
     if constexpr (kFp8) {
-      __builtin_amdgcn_s_waitcnt(0);
-      if (t + 2 < ntiles) f8_store(kst, kKBuf + kPar * kTileBytes, true);
-      f8_store(vst, kVBuf + (kPar ^ 1) * kTileBytes, false);
+      // K(t + 2) into stage t % 2 (K(t) there was last read in iteration t - 1), V(t + 1)
+      // into stage (t + 1) % 2 (V(t - 1) there likewise)
+      f8_store(kst, kKBase + kJ * kTileBytes, true);
+      f8_store(vst, kVBase + ((kJ + 1) % 2) * kTileBytes, false);
     }
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
   };
 
-  // Every load issued so far is complete here on every path (also ntiles == 0, which skips
-  // the block above): otherwise the compiler's bookkeeping keeps the Q loads pending at the
-  // loop head and waits for all vector memory, LDS-direct copies included, in each step.
-  __builtin_amdgcn_s_waitcnt(0);
-  int t = 0;
-  for (; t + 2 < ntiles; t += 2) {
-    iteration(t, std::integral_constant<int, 0>{});
-    iteration(t + 1, std::integral_constant<int, 1>{});
+  // Page ids of the first tiles are requested while the Q loads are in flight; the Q loads
+  // are then waited for on every path, before any LDS-direct copy is issued: the compiler's
+  // wait-count bookkeeping does not see those copies, and a Q load it still counted as
+  // pending would make it wait for every copy in each step of the loop.
+  wait_vmcnt<0>();
+  int32_t pg[kS + 1];
+#pragma unroll
+  for (int j = 0; j <= kS; ++j) pg[j] = page_of(j);
+  if (ntiles > 64 - kS - 2) fetch_window(64, 0);
+
+  if (ntiles > 0) {
+    // Prologue: copies K(0), V(0), K(1), V(1), ..., K(kS - 2), V(kS - 2), K(kS - 1); waits
+    // for K(0); sub-block 0 sets the reference to its own max (a lane with no visible key
+    // there has none in the group's range, as its visible keys form a prefix of it).
+    if constexpr (!kFp8) {
+#pragma unroll
+      for (int j = 0; j < kS - 1; ++j) {
+        dma_rows(kpb, pg[j], lo + j * kKvTile, kKBase + j * kTileBytes, kvo);
+        dma_rows(vpb, pg[j], lo + j * kKvTile, kVBase + j * kTileBytes, vvo);
+      }
+      dma_rows(kpb, pg[kS - 1], lo + (kS - 1) * kKvTile, kKBase + (kS - 1) * kTileBytes, kvo);
+      pg_klast = pg[kS - 1];
+      pg_knext = pg[kS];
+      wait_vmcnt<(2 * kS - 2) * kDma>();   // K(0), the first of these copies
+    } else {
+      const int32_t pg0 = pg[0], pg1 = pg[1];
+      f8_load(kst, kpb, pg0, lo, kvo);
+      f8_load(vst, vpb, pg0, lo, vvo);
+      f8_store(kst, kKBase, true);
+      f8_store(vst, kVBase, false);
+      f8_load(kst, kpb, pg1, lo + kKvTile, kvo);
+      f8_store(kst, kKBase + kTileBytes, true);
+      pg_klast = pg1;
+      pg_knext = pg[2];
+      wait_lgkmcnt0();
+    }
+    __builtin_amdgcn_s_barrier();
+
+    sp = qk(kKBase);
+    mask(sp, lo);
+    {
+      const float t = block_max(sp) * c_log2;
+      m_run = t == -INFINITY ? 0.f : t;
+    }
+    probs(sp, pa, lsum_p);
+    sc = qk(kKBase + kSubBytes);
   }
-  if (t + 1 < ntiles) {
-    iteration(t, std::integral_constant<int, 0>{});
-    ++t;
+
+  int t = 0;
+  if constexpr (kS == 4) {
+    for (; t + 4 < ntiles; t += 4) {
+      iteration(t, std::integral_constant<int, 0>{});
+      iteration(t + 1, std::integral_constant<int, 1>{});
+      iteration(t + 2, std::integral_constant<int, 2>{});
+      iteration(t + 3, std::integral_constant<int, 3>{});
+    }
+    if (t + 1 < ntiles) {
+      iteration(t, std::integral_constant<int, 0>{});
+      ++t;
+      if (t + 1 < ntiles) {
+        iteration(t, std::integral_constant<int, 1>{});
+        ++t;
+        if (t + 1 < ntiles) {
+          iteration(t, std::integral_constant<int, 2>{});
+          ++t;
+        }
+      }
+    }
+  } else {
+    for (; t + 2 < ntiles; t += 2) {
+      iteration(t, std::integral_constant<int, 0>{});
+      iteration(t + 1, std::integral_constant<int, 1>{});
+    }
+    if (t + 1 < ntiles) {
+      iteration(t, std::integral_constant<int, 0>{});
+      ++t;
+    }
   }
   if (ntiles > 0) {
     // last tile (t = ntiles - 1): sub-block 2t+1 takes the softmax, P(2t) V, then P(2t+1) V
-    const int vlast = kVBuf + (t & 1) * kTileBytes;
+    if constexpr (!kFp8) wait_vmcnt<0>();
+    else wait_lgkmcnt0();
+    __builtin_amdgcn_s_barrier();
+    const int vlast = kVBase + (t % kS) * kTileBytes;
     constexpr std::false_type kNoQK{};
     const Pre f = prefetch(0, vlast, kNoQK);
     settle(sp, pa, lsum_p);
     mask(sc, lo + (2 * t + 1) * 32);
-    Sums ls;
+    float ls;
     step_main(sc, pa, pb, 0, vlast, f, kNoQK, ls);
     settle(sc, pb, ls);
     pv_acc(pb, vlast + kSubBytes);
   }
 
-  const float lb_tot = sum_with_partner(l_run.b);
-  const float lf_tot = sum_with_partner(l_run.f);
+  float l_fin = sum_with_partner(l_run);
+  float m_fin = l_fin > 0.f ? m_run : -INFINITY;     // -inf: no visible key in this range
+  if constexpr (kHalves == 2) {
+    // The second group's (O, m, l) to the first through LDS (the rings are free once every
+    // wave is past its last tile): column wave cw of both groups holds the same elements in
+    // the same lanes; element group k = 4 db + j of lane l is at ((k kColWaves + cw) 64 + l)
+    // x 16 bytes, so each store or load of 64 lanes covers 1 KiB without bank conflicts.
+    __builtin_amdgcn_s_barrier();
+    float* xo = reinterpret_cast<float*>(smem);
+    float* xml = xo + 16 * kColWaves * 64 * 4;
+    if (grp == 1) {
+#pragma unroll
+      for (int db = 0; db < 4; ++db)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<f32x4*>(xo + (((4 * db + j) * kColWaves + cw) * 64 + lane) * 4) =
+              f32x4{o[db][4 * j], o[db][4 * j + 1], o[db][4 * j + 2], o[db][4 * j + 3]};
+      *reinterpret_cast<f32x2*>(xml + (cw * 64 + lane) * 2) = f32x2{m_fin, l_fin};
+    }
+    wait_lgkmcnt0();
+    __builtin_amdgcn_s_barrier();
+    if (grp == 1) return;
+    const f32x2 ml1 = *reinterpret_cast<const f32x2*>(xml + (cw * 64 + lane) * 2);
+    const float mstar = fmaxf(m_fin, ml1[0]);
+    const float a0 = merge_weight(m_fin, mstar), a1 = merge_weight(ml1[0], mstar);
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const f32x4 x = *reinterpret_cast<const f32x4*>(xo + (((4 * db + j) * kColWaves + cw) * 64 + lane) * 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) o[db][4 * j + e] = a0 * o[db][4 * j + e] + a1 * x[e];
+      }
+    l_fin = a0 * l_fin + a1 * ml1[1];
+    m_fin = mstar;
+  }
   if (!valid) return;
   if (ns == 1) {
-    const float inv = v_mul / lb_tot;
+    const float inv = v_mul / l_fin;
     uint16_t* orow = out + ((int64_t)(row0 + tok) * hq + hq_col) * 128 + 4 * half;
 #pragma unroll
     for (int db = 0; db < 4; ++db)
@@ -574,33 +693,43 @@ __global__ __launch_bounds__(kWaves * 64, 8 / kWaves) void attn_main_kernel(
                          pack_bf16x2(o[db][4 * j + 2] * inv, o[db][4 * j + 3] * inv)};
         *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * j) = w;
       }
-    if (lse != nullptr && half == 0) lse[(int64_t)(row0 + tok) * hq + hq_col] = (m_run + __log2f(lf_tot)) * kLn2;
-  } else {
-    float* acc = pv.partials + pv.part_off[r];
-    float* ml = acc + (int64_t)ns * C * hq * kHeadDim;
-    const int64_t prow = ((int64_t)it.s * C + tok) * hq + hq_col;
-    float* arow = acc + prow * kHeadDim + 4 * half;
-#pragma unroll
-    for (int db = 0; db < 4; ++db)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const f32x4 w = {o[db][4 * j] * v_mul, o[db][4 * j + 1] * v_mul, o[db][4 * j + 2] * v_mul,
-                         o[db][4 * j + 3] * v_mul};
-        *reinterpret_cast<f32x4*>(arow + 32 * db + 8 * j) = w;
-      }
-    // (m, l_b, l_f, 0); a column with no visible key in this piece has (-inf, 0, 0): the
-    // merge skips it
-    if (half == 0)
-      *reinterpret_cast<f32x4*>(ml + 4 * prow) = f32x4{lf_tot > 0.f ? m_run : -INFINITY, lb_tot, lf_tot, 0.f};
+    if (lse != nullptr && half == 0) lse[(int64_t)(row0 + tok) * hq + hq_col] = (m_fin + __log2f(l_fin)) * kLn2;
+    return;
   }
+  // Split piece: fp32 partial (acc row, then (m, l, 0, 0)); a column with no visible key in
+  // this piece has (-inf, 0): the merge skips it.
+  float* acc = pv.partials + it.part_off;
+  float* ml = acc + (int64_t)ns * C * hq * kHeadDim;
+  const int64_t prow = ((int64_t)it.s * C + tok) * hq + hq_col;
+  float* arow = acc + prow * kHeadDim + 4 * half;
+#pragma unroll
+  for (int db = 0; db < 4; ++db)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const f32x4 w = {o[db][4 * j] * v_mul, o[db][4 * j + 1] * v_mul, o[db][4 * j + 2] * v_mul,
+                       o[db][4 * j + 3] * v_mul};
+      *reinterpret_cast<f32x4*>(arow + 32 * db + 8 * j) = w;
+    }
+  if (half == 0) *reinterpret_cast<f32x4*>(ml + 4 * prow) = f32x4{m_fin, l_fin, 0.f, 0.f};
+}
+
+// Largest r with a[r] <= x, for a non-decreasing a[0..n] with a[0] <= x < a[n].
+__device__ inline int upper_index(const int32_t* a, int n, int x) {
+  int lo = 0, hi = n;  // invariant: a[lo] <= x < a[hi]
+  while (hi - lo > 1) {
+    int mid = (lo + hi) >> 1;
+    if (a[mid] <= x) lo = mid; else hi = mid;
+  }
+  return lo;
 }
 
 // Merge of split partials: workgroup (row, y) merges heads 8y .. 8y+7 of one chunk row;
-// each thread owns 4 dims of one head.
+// each thread owns 4 dims of one head.  Up to kFastPieces pieces are read in one round trip.
+constexpr int kFastPieces = 8;
 __global__ __launch_bounds__(256) void split_reduce_kernel(uint16_t* __restrict__ out, float* __restrict__ lse,
                                                            PlanPtrs pv, int32_t num_reqs, int32_t hq) {
   const int row = blockIdx.x;
-  if (num_reqs == 0 || row >= pv.cu[num_reqs]) return;
+  if (num_reqs == 0 || pv.hdr->status != 0 || row >= pv.cu[num_reqs]) return;
   const int r = upper_index(pv.cu, num_reqs, row);
   const int ns = pv.ns[r];
   if (ns <= 1) return;
@@ -611,56 +740,76 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(uint16_t* __restrict_
   const int u = blockIdx.y * 256 + threadIdx.x;
   if (u < hq * 32) {
     const int h = u >> 5, d4 = (u & 31) * 4;
-    float mstar = -INFINITY;
-    for (int s = 0; s < ns; ++s) mstar = fmaxf(mstar, ml[4 * (((int64_t)s * C + tok) * hq + h)]);
-    float lb = 0.f, lf = 0.f;
+    const int64_t piece = (int64_t)C * hq;                 // rows of one piece
+    const int64_t prow0 = (int64_t)tok * hq + h;
+    float mstar = -INFINITY, lb = 0.f;
     f32x4 a = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < ns; ++s) {
-      const int64_t prow = ((int64_t)s * C + tok) * hq + h;
-      const f32x4 mlp = *reinterpret_cast<const f32x4*>(ml + 4 * prow);
-      if (mlp[0] == -INFINITY) continue;
-      const float wgt = __builtin_amdgcn_exp2f(mlp[0] - mstar);
-      lb += wgt * mlp[1];
-      lf += wgt * mlp[2];
-      const f32x4 x = *reinterpret_cast<const f32x4*>(acc + prow * kHeadDim + d4);
-      a += wgt * x;
+    if (ns <= kFastPieces) {
+      // every piece's (m, l) and values loaded at once (one round trip)
+      f32x4 mls[kFastPieces], xs[kFastPieces];
+#pragma unroll
+      for (int s = 0; s < kFastPieces; ++s)
+        if (s < ns) {
+          mls[s] = *reinterpret_cast<const f32x4*>(ml + 4 * (s * piece + prow0));
+          xs[s] = *reinterpret_cast<const f32x4*>(acc + (s * piece + prow0) * kHeadDim + d4);
+        }
+#pragma unroll
+      for (int s = 0; s < kFastPieces; ++s)
+        if (s < ns) mstar = fmaxf(mstar, mls[s][0]);
+#pragma unroll
+      for (int s = 0; s < kFastPieces; ++s)
+        if (s < ns && mls[s][0] != -INFINITY) {
+          const float wgt = merge_weight(mls[s][0], mstar);
+          lb += wgt * mls[s][1];
+          a += wgt * xs[s];
+        }
+    } else {
+      for (int s = 0; s < ns; ++s) mstar = fmaxf(mstar, ml[4 * (s * piece + prow0)]);
+      for (int s = 0; s < ns; ++s) {
+        const int64_t prow = s * piece + prow0;
+        const f32x4 mlp = *reinterpret_cast<const f32x4*>(ml + 4 * prow);
+        if (mlp[0] == -INFINITY) continue;
+        const float wgt = merge_weight(mlp[0], mstar);
+        lb += wgt * mlp[1];
+        a += wgt * *reinterpret_cast<const f32x4*>(acc + prow * kHeadDim + d4);
+      }
     }
     const float inv = 1.0f / lb;
     const u32x2 w = {pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv)};
     *reinterpret_cast<u32x2*>(out + ((int64_t)row * hq + h) * kHeadDim + d4) = w;
-    if (lse != nullptr && d4 == 0) lse[(int64_t)row * hq + h] = (mstar + __log2f(lf)) * kLn2;
+    if (lse != nullptr && d4 == 0) lse[(int64_t)row * hq + h] = (mstar + __log2f(lb)) * kLn2;
   }
 }
 
 }  // namespace
 
-template <bool kFp8, int kWaves>
+template <bool kFp8, int kColWaves, int kHalves>
 void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
-  attn_main_kernel<kFp8, kWaves><<<a.num_items, kWaves * 64, 0, stream>>>(
+  attn_main_kernel<kFp8, kColWaves, kHalves><<<(unsigned)a.dims.num_items, kColWaves * kHalves * 64, 0, stream>>>(
       static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
-      a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.kv.num_reqs, a.hq, a.kv.hkv,
-      a.softmax_scale * kLog2e, plan_ptrs(a.workspace, a.kv.num_reqs));
+      a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, a.softmax_scale * kLog2e,
+      plan_ptrs(a.workspace, a.dims));
+}
+
+template <bool kFp8>
+void launch_main_dtype(const AttnLaunch& a, hipStream_t stream) {
+  if (a.tile_cols == kMaxTileCols) launch_main_variant<kFp8, 8, 1>(a, stream);
+  else if (a.key_halves == 2) launch_main_variant<kFp8, 4, 2>(a, stream);
+  else launch_main_variant<kFp8, 4, 1>(a, stream);
 }
 
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream) {
-  if (a.num_items <= 0) return hipSuccess;
-  const bool wide = a.tile_cols == kMaxTileCols;
-  if (a.kv.fp8) {
-    if (wide) launch_main_variant<true, 8>(a, stream);
-    else launch_main_variant<true, 4>(a, stream);
-  } else {
-    if (wide) launch_main_variant<false, 8>(a, stream);
-    else launch_main_variant<false, 4>(a, stream);
-  }
+  if (a.dims.num_items <= 0) return hipSuccess;
+  if (a.kv.fp8) launch_main_dtype<true>(a, stream);
+  else launch_main_dtype<false>(a, stream);
   return hipGetLastError();
 }
 
 hipError_t launch_split_reduce(const ReduceLaunch& a, hipStream_t stream) {
   if (a.total_tokens <= 0) return hipSuccess;
   dim3 grid((unsigned)a.total_tokens, (unsigned)((a.hq * 32 + 255) / 256));
-  split_reduce_kernel<<<grid, 256, 0, stream>>>(
-      static_cast<uint16_t*>(a.out), a.lse, plan_ptrs(const_cast<void*>(a.workspace), a.num_reqs), a.num_reqs,
-      a.hq);
+  split_reduce_kernel<<<grid, 256, 0, stream>>>(static_cast<uint16_t*>(a.out), a.lse,
+                                                plan_ptrs(const_cast<void*>(a.workspace), a.dims), a.num_reqs, a.hq);
   return hipGetLastError();
 }
 

@@ -4,9 +4,10 @@
 // p % 16; the block table maps logical pages to physical ones.  Append (Sec. 4.2 /
 // Sec. 5.1): a chunk of C new tokens after P cached ones occupies positions P .. P+C-1.
 //
-// One workgroup per (request, logical page touched).  A page of one kv head is a
-// contiguous 4 KiB (bf16) / 2 KiB (fp8) run; a wave writes four 256-byte slot rows of it
-// per instruction, reading the matching rows of the [T][Hkv][128] input.
+// Append: one workgroup per (logical page touched, kv head, request).  A page of one kv head
+// is a contiguous 4 KiB (bf16) / 2 KiB (fp8) run of 16 slot rows; thread t moves 16 bytes
+// of input (8 elements) of slot t / 16, chunk t % 16, for K and for V: one load and one
+// store each, coalesced on both sides (a slot row is 256 contiguous input bytes).
 #include "launch.h"
 #include "s2l_device.h"
 
@@ -21,37 +22,33 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
     const int32_t* __restrict__ prefix_lens, const int32_t* __restrict__ chunk_lens,
     const int32_t* __restrict__ cu_chunk, const int32_t* __restrict__ block_tables, int32_t max_pages,
     int32_t hkv) {
-  const int r = blockIdx.y;
+  const int r = blockIdx.z, h = blockIdx.y;
   const int P = prefix_lens[r], C = chunk_lens[r];
   if (C <= 0) return;
   const int lp = (P >> 4) + (int)blockIdx.x;
   if (lp > ((P + C - 1) >> 4)) return;
-  const int row0 = cu_chunk[r];
+  const int slot = threadIdx.x >> 4, c = threadIdx.x & 15;
+  const int pos = lp * 16 + slot;
+  if (pos < P || pos >= P + C) return;
   const int64_t page = block_tables[(int64_t)r * max_pages + lp];
-  const int units = hkv * 256;  // kv heads x 16 slots x 16 chunks of 8 elements
-  for (int u = threadIdx.x; u < units; u += 256) {
-    const int c = u & 15, slot = (u >> 4) & 15, h = u >> 8;
-    const int pos = lp * 16 + slot;
-    if (pos < P || pos >= P + C) continue;
-    const int64_t src = ((int64_t)(row0 + pos - P) * hkv + h) * 128 + c * 8;
-    const int64_t dst = ((page * hkv + h) * 16 + slot) * 128 + c * 8;
-    const u32x4 kx = *reinterpret_cast<const u32x4*>(knew + src);
-    const u32x4 vx = *reinterpret_cast<const u32x4*>(vnew + src);
-    if constexpr (!kFp8) {
-      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(kpool) + dst) = kx;
-      *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(vpool) + dst) = vx;
-    } else {
-      // code = e4m3(fp32(x) * fp32(1/scale[h])), RNE, saturated
-      const float ki = __fdiv_rn(1.0f, kscale[h]);
-      const float vi = __fdiv_rn(1.0f, vscale[h]);
-      u32x2 kq, vq;
-      kq[0] = f32x4_to_fp8x4(bf16lo(kx[0]) * ki, bf16hi(kx[0]) * ki, bf16lo(kx[1]) * ki, bf16hi(kx[1]) * ki);
-      kq[1] = f32x4_to_fp8x4(bf16lo(kx[2]) * ki, bf16hi(kx[2]) * ki, bf16lo(kx[3]) * ki, bf16hi(kx[3]) * ki);
-      vq[0] = f32x4_to_fp8x4(bf16lo(vx[0]) * vi, bf16hi(vx[0]) * vi, bf16lo(vx[1]) * vi, bf16hi(vx[1]) * vi);
-      vq[1] = f32x4_to_fp8x4(bf16lo(vx[2]) * vi, bf16hi(vx[2]) * vi, bf16lo(vx[3]) * vi, bf16hi(vx[3]) * vi);
-      *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(kpool) + dst) = kq;
-      *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(vpool) + dst) = vq;
-    }
+  const int64_t src = ((int64_t)(cu_chunk[r] + pos - P) * hkv + h) * 128 + c * 8;
+  const int64_t dst = ((page * hkv + h) * 16 + slot) * 128 + c * 8;
+  const u32x4 kx = *reinterpret_cast<const u32x4*>(knew + src);
+  const u32x4 vx = *reinterpret_cast<const u32x4*>(vnew + src);
+  if constexpr (!kFp8) {
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(kpool) + dst) = kx;
+    *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(vpool) + dst) = vx;
+  } else {
+    // code = e4m3(fp32(x) * fp32(1/scale[h])), RNE, saturated
+    const float ki = __fdiv_rn(1.0f, kscale[h]);
+    const float vi = __fdiv_rn(1.0f, vscale[h]);
+    u32x2 kq, vq;
+    kq[0] = f32x4_to_fp8x4(bf16lo(kx[0]) * ki, bf16hi(kx[0]) * ki, bf16lo(kx[1]) * ki, bf16hi(kx[1]) * ki);
+    kq[1] = f32x4_to_fp8x4(bf16lo(kx[2]) * ki, bf16hi(kx[2]) * ki, bf16lo(kx[3]) * ki, bf16hi(kx[3]) * ki);
+    vq[0] = f32x4_to_fp8x4(bf16lo(vx[0]) * vi, bf16hi(vx[0]) * vi, bf16lo(vx[1]) * vi, bf16hi(vx[1]) * vi);
+    vq[1] = f32x4_to_fp8x4(bf16lo(vx[2]) * vi, bf16hi(vx[2]) * vi, bf16lo(vx[3]) * vi, bf16hi(vx[3]) * vi);
+    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(kpool) + dst) = kq;
+    *reinterpret_cast<u32x2*>(static_cast<uint8_t*>(vpool) + dst) = vq;
   }
 }
 
@@ -90,7 +87,7 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(
 hipError_t launch_kv_append(const KvLaunch& a, const void* knew, const void* vnew, int32_t max_pages_touched,
                             hipStream_t stream) {
   if (a.num_reqs == 0 || max_pages_touched == 0) return hipSuccess;
-  dim3 grid(max_pages_touched, a.num_reqs);
+  dim3 grid(max_pages_touched, a.hkv, a.num_reqs);
   if (a.fp8) {
     kv_append_kernel<true><<<grid, 256, 0, stream>>>(
         a.kpool, a.vpool, a.kscale, a.vscale, static_cast<const uint16_t*>(knew),

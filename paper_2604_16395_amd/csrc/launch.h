@@ -3,6 +3,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "plan_rules.h"
+
 namespace s2l {
 
 struct KvLaunch {           // device pointers of one layer's cache and one batch
@@ -30,11 +32,11 @@ struct PlanLaunch {
   const int32_t* chunk_lens;
   const int32_t* cu_chunk;
   int32_t num_reqs, hq, hkv;
-  int32_t target_items, min_split_keys, max_splits, tile_cols;
+  int32_t split_keys, max_splits, tile_cols;   // split_keys chosen by the host planner
   int64_t ws_bytes;
   void* workspace;
 };
-hipError_t launch_attn_plan(const PlanLaunch& a, hipStream_t stream);
+hipError_t launch_attn_plan(const PlanLaunch& a, const PlanDims& dims, hipStream_t stream);
 
 struct AttnLaunch {
   KvLaunch kv;
@@ -44,8 +46,9 @@ struct AttnLaunch {
   int32_t hq;
   float softmax_scale;
   void* workspace;
-  int32_t num_items;        // grid size (host copy of the plan's item count)
+  PlanDims dims;            // host copy of the plan's sizes (grid = dims.num_items)
   int32_t tile_cols;        // 128 or 256 (host copy of the plan's tile width)
+  int32_t key_halves;       // 1 or 2 wave groups per item, each on half of its key range
 };
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream);
 
@@ -56,6 +59,7 @@ struct ReduceLaunch {
   int32_t hq;
   int32_t num_reqs;
   int64_t total_tokens;
+  PlanDims dims;
 };
 hipError_t launch_split_reduce(const ReduceLaunch& a, hipStream_t stream);
 

@@ -27,8 +27,15 @@ constexpr int kKvTile = 64;         // keys per LDS tile
 constexpr int kMaxSplitsCap = 64;
 constexpr int kDefaultMinSplitKeys = 512;
 constexpr int kDefaultMaxSplits = 16;
-constexpr int kDefaultItemsPerCu = 2;
 constexpr int32_t kPlanMagic = 0x53324c50;  // "S2LP"
+
+// Work items resident per CU: a 128-column item is a 4-wave workgroup with a two-stage
+// K/V ring (64 KiB of LDS), two per CU, or with two key-range groups an 8-wave workgroup
+// with two such rings (128 KiB), one per CU; a 256-column item is an 8-wave workgroup with
+// a four-stage ring (128 KiB), one per CU.
+S2L_HD inline int32_t items_per_cu(int32_t tile_cols, int32_t key_halves) {
+  return tile_cols == kMaxTileCols || key_halves == 2 ? 1 : 2;
+}
 
 struct PlanHeader {           // first 256 bytes of the workspace
   int32_t magic;
@@ -37,12 +44,22 @@ struct PlanHeader {           // first 256 bytes of the workspace
   int32_t num_items;
   int32_t num_split_reqs;
   int32_t split_keys;
-  int32_t status;             // 0 ok, 1 = partials exceed the workspace (nothing planned)
+  int32_t status;             // 0 ok, 1 = the device partition does not fit the host's sizing
   int32_t tile_cols;
-  int32_t pad1;
+  int32_t num_tiles;
   int64_t part_floats;
   int64_t total_tokens;
 };
+
+// One work item as the attention kernel reads it (a single 64-byte scalar load).
+struct ItemRec {
+  int32_t r, g, i0, i1;       // request, kv head, chunk tokens [i0, i1)
+  int32_t lo, hi, s, ns;      // key range [lo, hi), piece s of ns
+  int32_t p, c, row0, tile;   // P_r, C_r, first row of the request, query-tile index
+  int64_t part_off;           // floats: start of the request's partials
+  int32_t pad0, pad1;
+};
+static_assert(sizeof(ItemRec) == 64, "ItemRec is one 64-byte scalar load");
 
 // a must be a power of two
 S2L_HD inline int64_t align_up(int64_t x, int64_t a) {
@@ -54,27 +71,8 @@ S2L_HD inline int64_t ceil_div64(int64_t a, int64_t b) { return (a + b - 1) / b;
 S2L_HD inline int32_t tile_tokens(int32_t g, int32_t tile_cols) { return tile_cols / g; }
 S2L_HD inline int32_t num_qtiles(int32_t c, int32_t tq) { return c > 0 ? ceil_div(c, tq) : 0; }
 
-// Keys summed over the query tiles of one (request, kv head): tile t covers tokens
-// [t*tq, min((t+1)*tq, C)) and reads keys [0, P + min((t+1)*tq, C)).
-S2L_HD inline int64_t req_work(int32_t p, int32_t c, int32_t tq) {
-  int64_t n = num_qtiles(c, tq);
-  if (n == 0) return 0;
-  return n * (int64_t)p + (int64_t)tq * (n - 1) * n / 2 + c;
-}
-
-// Piece length (keys) for the batch: 0 (no split) when the batch already has at least
-// target_items tiles, else total keys / target_items, at least min_split_keys, rounded
-// up to a multiple of kKvTile.
-S2L_HD inline int32_t split_keys_for(int64_t base_items, int64_t total_work, int32_t target_items,
-                                     int32_t min_split_keys) {
-  if (base_items >= target_items || base_items == 0) return 0;
-  int64_t l = ceil_div64(total_work, target_items);
-  if (l < min_split_keys) l = min_split_keys;
-  l = align_up(l, kKvTile);
-  if (l > (int64_t)1 << 30) l = (int64_t)1 << 30;
-  return (int32_t)l;
-}
-
+// Pieces of a request with piece length split_keys (0 = no split): every tile of the
+// request is cut into the same number, set by its longest key range [0, P + C).
 S2L_HD inline int32_t req_splits(int32_t p, int32_t c, int32_t split_keys, int32_t max_splits) {
   if (split_keys <= 0 || c <= 0) return 1;
   int64_t n = ceil_div64((int64_t)p + c, split_keys);
@@ -93,41 +91,46 @@ S2L_HD inline void piece_range(int32_t kv_end, int32_t ns, int32_t s, int32_t* l
 }
 
 // Floats of split partials for one request: ns pieces x C rows x Hq heads x (D + 4): the
-// unnormalised output row, then (m, l_b, l_f, 0) per row.
+// unnormalised output row, then (m, l, 0, 0) per row.
 S2L_HD inline int64_t req_part_floats(int32_t ns, int32_t c, int32_t hq) {
   return ns > 1 ? (int64_t)ns * c * hq * (kHeadDim + 4) : 0;
 }
 
-// Workspace layout (byte offsets), a function of R only.
+// Workspace layout (byte offsets), a function of the request count R, the item count W,
+// the tile count NT and the partial floats (all four known to the host planner).
 struct PlanLayout {
-  int64_t item_off;   // int32 [R+1]
-  int64_t nqt;        // int32 [R]
-  int64_t ns;         // int32 [R]
-  int64_t p;          // int32 [R]
+  int64_t item_off;   // int32 [R+1]   first item of each request
+  int64_t ns;         // int32 [R]     pieces per request
   int64_t c;          // int32 [R]
   int64_t cu;         // int32 [R+1]
   int64_t part_off;   // int64 [R]
+  int64_t items;      // ItemRec [W]
   int64_t partials;   // float [part_floats]
+  int64_t end;
 };
 
-S2L_HD inline PlanLayout plan_layout(int32_t r) {
+S2L_HD inline PlanLayout plan_layout(int32_t r, int64_t w, int64_t nt, int64_t part_floats) {
   PlanLayout L;
   int64_t o = 256;
   L.item_off = o; o += 4 * (int64_t)(r + 1);
-  L.nqt = o;      o += 4 * (int64_t)r;
   L.ns = o;       o += 4 * (int64_t)r;
-  L.p = o;        o += 4 * (int64_t)r;
   L.c = o;        o += 4 * (int64_t)r;
   L.cu = o;       o += 4 * (int64_t)(r + 1);
   o = align_up(o, 8);
   L.part_off = o; o += 8 * (int64_t)r;
+  o = align_up(o, 64);
+  L.items = o;    o += 64 * w;
+  (void)nt;
   L.partials = align_up(o, 256);
+  L.end = L.partials + align_up(part_floats * 4, 256);
   return L;
 }
 
-S2L_HD inline int64_t workspace_bytes_for(int32_t r, int64_t part_floats) {
-  return plan_layout(r).partials + align_up(part_floats * 4, 256);
-}
+// The sizes a plan was made for (host plan); the layout and every launch derive from them.
+struct PlanDims {
+  int32_t num_reqs;
+  int64_t num_items, num_tiles, part_floats;
+};
 
 // Typed pointers into a workspace, computed once on the host and passed to every kernel
 // by value.  (Kernels never rebuild them from the layout arithmetic: a scalar load whose
@@ -136,33 +139,34 @@ S2L_HD inline int64_t workspace_bytes_for(int32_t r, int64_t part_floats) {
 struct PlanPtrs {
   PlanHeader* hdr;
   int32_t* item_off;
-  int32_t* nqt;
   int32_t* ns;
-  int32_t* p;
   int32_t* c;
   int32_t* cu;
   int64_t* part_off;
+  ItemRec* items;
   float* partials;
+  int64_t cap_items, cap_tiles, cap_part_floats;   // sizes the workspace was laid out for
 };
 
-inline PlanPtrs plan_ptrs(void* ws, int32_t r) {
+inline PlanPtrs plan_ptrs(void* ws, const PlanDims& d) {
   char* b = static_cast<char*>(ws);
-  PlanLayout L = plan_layout(r);
+  PlanLayout L = plan_layout(d.num_reqs, d.num_items, d.num_tiles, d.part_floats);
   PlanPtrs q;
   q.hdr = reinterpret_cast<PlanHeader*>(b);
   q.item_off = reinterpret_cast<int32_t*>(b + L.item_off);
-  q.nqt = reinterpret_cast<int32_t*>(b + L.nqt);
   q.ns = reinterpret_cast<int32_t*>(b + L.ns);
-  q.p = reinterpret_cast<int32_t*>(b + L.p);
   q.c = reinterpret_cast<int32_t*>(b + L.c);
   q.cu = reinterpret_cast<int32_t*>(b + L.cu);
   q.part_off = reinterpret_cast<int64_t*>(b + L.part_off);
+  q.items = reinterpret_cast<ItemRec*>(b + L.items);
   q.partials = reinterpret_cast<float*>(b + L.partials);
+  q.cap_items = d.num_items;
+  q.cap_tiles = d.num_tiles;
+  q.cap_part_floats = d.part_floats;
   return q;
 }
 
-// Decode work item w of request r (local index = w - item_off[r]):
-// local = ((g * nqt) + t) * ns + s.
+// Decode the local index of an item within its request: local = ((g * nqt) + t) * ns + s.
 struct Item {
   int32_t g, qt, s;
 };

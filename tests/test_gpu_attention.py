@@ -13,6 +13,9 @@ from tests.gpu_util import (DEV, SCALE, Setup, assert_attention_close, bf16_to_f
 pytestmark = pytest.mark.gpu
 
 FORCE_SPLIT = dict(target_items=1 << 20, min_split_keys=64, max_splits=16)
+# (tile_cols, key_halves): 4-wave workgroups, 8-wave workgroups of two key-range groups,
+# 8-wave workgroups of 256 columns
+LAYOUTS = [(128, 1), (128, 2), (256, 1)]
 
 SMALL = [
     ("cfg1", [256], [128], 8, 2),
@@ -26,16 +29,16 @@ SMALL = [
 ]
 
 
-@pytest.mark.parametrize("tile_cols", [128, 256])
+@pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("name,P,C,hq,hkv", SMALL)
-def test_small_cases_match_oracle(name, P, C, hq, hkv, split, tile_cols):
+def test_small_cases_match_oracle(name, P, C, hq, hkv, split, layout):
     case = workloads.make_case(name, P, C, hq, hkv, seed=zlib.crc32(name.encode()) % 1000)
-    print(f"[attn] {name} split={split} tile_cols={tile_cols}", flush=True)
+    print(f"[attn] {name} split={split} layout={layout}", flush=True)
     s = Setup(case)
     s.append()
     opts = dict(FORCE_SPLIT) if split else {}
-    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols, **opts))
+    out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1], **opts))
     if split and max(P) + max(C) > 64:
         assert s.plan.num_split_reqs > 0
     ref = s.oracle()
@@ -65,8 +68,8 @@ def test_peaky_and_growing_scores(q_sigma, k_ramp):
     during the key loop and the rescaling path runs), and near-uniform scores."""
     case = workloads.make_case("peaky", [3000, 100], [300, 64], 32, 8, seed=10, q_sigma=q_sigma,
                                k_ramp=k_ramp)
-    for opts in (None, s2l.plan_opts(**FORCE_SPLIT), s2l.plan_opts(tile_cols=256),
-                 s2l.plan_opts(tile_cols=256, **FORCE_SPLIT)):
+    for opts in [None] + [s2l.plan_opts(tile_cols=t, key_halves=h, **extra) for t, h in LAYOUTS
+                          for extra in ({}, FORCE_SPLIT)]:
         s = Setup(case)
         s.append()
         out, lse = s.attention(opts)
@@ -74,12 +77,12 @@ def test_peaky_and_growing_scores(q_sigma, k_ramp):
         assert_attention_close(case, out, lse, ref, what=f"peaky{q_sigma},{k_ramp}")
 
 
-@pytest.mark.parametrize("tile_cols", [128, 256])
-def test_config2_sampled_rows(tile_cols):
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_config2_sampled_rows(layout):
     case = workloads.config2()
     s = Setup(case)
     s.append()
-    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols))
+    out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1]))
     rows = sample_rows(case, 48, np.random.default_rng(2))
     ref = s.oracle(rows)
     assert_attention_close(case, out, lse, ref, rows, what="cfg2")
@@ -95,12 +98,12 @@ def test_config4_mixed_batch_sampled_rows():
     assert_attention_close(case, out, lse, ref, rows, what="cfg4")
 
 
-@pytest.mark.parametrize("tile_cols", [128, 256])
-def test_config5_fp8_cache_sampled_rows(tile_cols):
+@pytest.mark.parametrize("layout", [(128, 2), (256, 1)])
+def test_config5_fp8_cache_sampled_rows(layout):
     case = workloads.config5()
     s = Setup(case)
     s.append()
-    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols))
+    out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1]))
     rows = sample_rows(case, 30, np.random.default_rng(5))
     ref = s.oracle(rows)
     assert_attention_close(case, out, lse, ref, rows, what="cfg5")
@@ -127,13 +130,13 @@ def test_empty_and_zero_length_requests():
     assert plan.num_items == 0
 
 
-@pytest.mark.parametrize("tile_cols", [128, 256])
+@pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("split", [False, True])
-def test_small_fp8_cache_matches_oracle(split, tile_cols):
+def test_small_fp8_cache_matches_oracle(split, layout):
     case = workloads.make_case("fp8_small", [700, 0, 33], [130, 77, 1], 64, 8, seed=14, kv_dtype="fp8")
     s = Setup(case)
     s.append()
     opts = dict(FORCE_SPLIT) if split else {}
-    out, lse = s.attention(s2l.plan_opts(tile_cols=tile_cols, **opts))
+    out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1], **opts))
     ref = s.oracle()
     assert_attention_close(case, out, lse, ref, what="fp8_small")

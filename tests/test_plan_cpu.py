@@ -11,7 +11,7 @@ from paper_2604_16395_amd import plan_opts, s2l_plan_host
 import workloads
 
 
-def _coverage(P, C, hq, hkv, items):
+def _coverage(P, C, hq, hkv, items, tile_cols):
     G = hq // hkv
     for r in range(len(P)):
         for g in range(hkv):
@@ -19,9 +19,9 @@ def _coverage(P, C, hq, hkv, items):
             if C[r] == 0:
                 assert len(mine) == 0
                 continue
-            # query tiles partition [0, C) with tq = 128 // G tokens
+            # query tiles partition [0, C) with tq = tile_cols // G tokens
             tiles = sorted({(int(a), int(b)) for a, b in mine[:, 2:4]})
-            tq = 128 // G
+            tq = tile_cols // G
             assert tiles == [(t, min(t + tq, C[r])) for t in range(0, C[r], tq)]
             for (i0, i1) in tiles:
                 pcs = mine[(mine[:, 2] == i0)]
@@ -38,19 +38,25 @@ def _coverage(P, C, hq, hkv, items):
                 assert P[r] + i1 - 1 < len(cover) + 1
 
 
+@pytest.mark.parametrize("tile_cols,halves", [(0, 0), (128, 1), (256, 0)])
 @pytest.mark.parametrize("target", [1, 64, 1 << 20])
 @pytest.mark.parametrize("hq,hkv", [(8, 2), (32, 8), (6, 2), (4, 4), (64, 8)])
-def test_items_cover_each_visible_pair_once(target, hq, hkv):
+def test_items_cover_each_visible_pair_once(target, hq, hkv, tile_cols, halves):
     rng = np.random.default_rng(target + hq)
     P = rng.integers(0, 3000, size=7).astype(np.int32)
     C = rng.integers(0, 300, size=7).astype(np.int32)
     P[0], C[0] = 0, 1
     C[1] = 0
     P[2] = 17
-    info, items = s2l_plan_host(P, C, hq, hkv, plan_opts(target_items=target, min_split_keys=64), with_items=True)
+    info, items = s2l_plan_host(P, C, hq, hkv, plan_opts(target_items=target, min_split_keys=64,
+                                                         tile_cols=tile_cols, key_halves=halves),
+                                with_items=True)
     assert info.num_items == len(items)
-    _coverage(P, C, hq, hkv, items)
+    assert tile_cols == 0 or info.tile_cols == tile_cols
+    _coverage(P, C, hq, hkv, items, info.tile_cols)
     assert info.total_tokens == C.sum()
+    # one tile per (request, kv head, query tile); the items of a tile are its pieces
+    assert info.num_tiles == len({(r, g, i0) for r, g, i0 in items[:, 0:3]})
 
 
 def test_plan_is_deterministic_and_independent_of_call():
@@ -61,24 +67,60 @@ def test_plan_is_deterministic_and_independent_of_call():
 
 
 def test_split_policy_on_the_named_workloads():
-    # one 512-token chunk at an 8K prefix: 128 tiles < 512 wanted -> the prefix is split
-    info, _ = s2l_plan_host([8192], [512], 32, 8, num_cus=256)
-    assert info.num_split_reqs == 1 and info.num_items >= 512 and info.split_keys % 64 == 0
-    # 8 x 512-token chunks: 1024 tiles already -> no split
+    # one 512-token chunk at an 8K prefix: 256-column tiles (64 tokens x 4 heads), 64 tiles
+    # for 256 one-per-CU workgroups -> every tile cut into 4 pieces: exactly 256 items
+    info, items = s2l_plan_host([8192], [512], 32, 8, num_cus=256, with_items=True)
+    assert info.tile_cols == 256 and info.key_halves == 1 and info.num_tiles == 64
+    assert info.num_split_reqs == 1 and info.num_items == 256 and info.split_keys % 64 == 0
+    assert set(items[:, 7]) == {4}
+    # 128-column tiles with two key-range wave groups, one workgroup per CU: 2 pieces
+    info, _ = s2l_plan_host([8192], [512], 32, 8, plan_opts(tile_cols=128), num_cus=256)
+    assert info.key_halves == 2 and info.num_tiles == 128 and info.num_items == 256
+    # 4-wave workgroups, two per CU: 128 tiles -> 4 pieces
+    info, _ = s2l_plan_host([8192], [512], 32, 8, plan_opts(tile_cols=128, key_halves=1), num_cus=256)
+    assert info.num_tiles == 128 and info.num_items == 512
+    # 8 x 512-token chunks: 512 tiles already -> no split
     P2, C2, _ = workloads.config2_lengths()
     info, _ = s2l_plan_host(P2, C2, 32, 8, num_cus=256)
-    assert info.num_split_reqs == 0 and info.num_items == 8 * 8 * 16
-    # 70B share: 2048 tokens x 8 heads / 16 tokens per tile = 1024 tiles -> no split
+    assert info.num_split_reqs == 0 and info.num_items == 8 * 8 * 8
+    # 70B share: 2048 tokens x 8 heads / 32 tokens per tile = 512 tiles -> no split
     info, _ = s2l_plan_host([131072], [2048], 64, 8, num_cus=256)
-    assert info.num_split_reqs == 0 and info.num_items == 1024
+    assert info.num_split_reqs == 0 and info.num_items == 512
+
+
+def test_automatic_tile_width():
+    # decode-like rows (C * G = 4 columns per kv head) fill 256-column tiles to 1.6%: 128
+    info, _ = s2l_plan_host([4000] * 16, [1] * 16, 32, 8, num_cus=256)
+    assert info.tile_cols == 128 and info.key_halves == 2
+    info, _ = s2l_plan_host([100, 5000], [300, 700], 32, 8, num_cus=256)
+    assert info.tile_cols == 256 and info.key_halves == 1
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_splitting_never_exceeds_the_target(seed):
+    rng = np.random.default_rng(seed)
+    R = int(rng.integers(1, 12))
+    P = rng.integers(0, 40000, size=R).astype(np.int32)
+    C = rng.integers(1, 700, size=R).astype(np.int32)
+    target = int(rng.integers(8, 600))
+    info, _ = s2l_plan_host(P, C, 32, 8, plan_opts(target_items=target, min_split_keys=64))
+    assert info.num_items <= max(target, info.num_tiles)
+
+
+def test_option_validation():
+    with pytest.raises(Exception):
+        s2l_plan_host([100], [10], 32, 8, plan_opts(tile_cols=256, key_halves=2))
+    with pytest.raises(Exception):
+        s2l_plan_host([100], [10], 32, 8, plan_opts(key_halves=3))
 
 
 def test_workspace_grows_with_partials_only_for_split_requests():
     a, _ = s2l_plan_host([8192], [512], 32, 8, num_cus=256)
     b, _ = s2l_plan_host([8192], [512], 32, 8, plan_opts(target_items=1), num_cus=256)
     assert b.num_split_reqs == 0 and b.workspace_bytes < a.workspace_bytes
-    ns = a.num_items // (8 * 16)
-    assert a.workspace_bytes >= ns * 512 * 32 * 130 * 4
+    ns = a.num_items // a.num_tiles
+    assert a.part_floats == ns * 512 * 32 * 132 and b.part_floats == 0
+    assert a.workspace_bytes >= ns * 512 * 32 * 132 * 4 + 64 * a.num_items
 
 
 def test_empty_and_degenerate_batches():
