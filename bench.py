@@ -103,6 +103,8 @@ def main():
                     help="wave groups per work item splitting its key range (0 = library default)")
     ap.add_argument("--target-items", type=int, default=0,
                     help="work items the planner aims for when splitting prefixes (0 = library default)")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch every kernel directly instead of through HIP graphs (for counter runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (for counter calibration) and exit")
@@ -173,7 +175,16 @@ def main():
 
     # Every launch is captured once into HIP graphs and replayed, so that the timed regions
     # measure the GPU, not the host's launch rate.
+    class Eager:   # stands in for a graph under --eager: replay() runs the launches again
+        def __init__(self, fn):
+            self.fn = fn
+
+        def replay(self):
+            self.fn()
+
     def capture(fn):
+        if args.eager:
+            return Eager(fn)
         g = torch.cuda.CUDAGraph()
         with torch.cuda.stream(main_stream):
             with torch.cuda.graph(g, stream=main_stream):
@@ -259,8 +270,9 @@ def main():
         "us_per_chunk": round(ms_per_step * 1e3, 2),
         "pct_mfma_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "step_breakdown_us": step_breakdown,
-        "timing": "one HIP graph of the K steps, replayed once; per-kernel times are averages over "
-                  "graphs of back-to-back launches of that kernel",
+        "timing": ("direct launches (--eager)" if args.eager else
+                   "one HIP graph of the K steps, replayed once; per-kernel times are averages over "
+                   "graphs of back-to-back launches of that kernel"),
         "plan": {"work_items": plan.num_items, "split_requests": plan.num_split_reqs,
                  "split_keys": plan.split_keys, "tile_cols": plan.tile_cols, "key_halves": plan.key_halves},
         "wall_s_timed_region": round(wall, 4),
