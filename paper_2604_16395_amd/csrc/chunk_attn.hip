@@ -380,10 +380,13 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   };
   // Pipelined step in eight slots; slot i issues S(b+1) += K_i Q_i (k-step i), O_db +=
   // V^T P(b-1) (k2 = i / 4, db = i % 4) and the probabilities of score elements 2i, 2i+1
-  // of sub-block b, while the operands of slot i + 2 are read from LDS.
+  // of sub-block b, while the operands of slot i + 2 are read from LDS.  With a next step
+  // in the same tile (with_next), slots 6 and 7 also read that step's first two operands
+  // (at nkofs / nvofs) into nxt, so its reads are not exposed behind its softmax prologue.
   auto step_main = [&](const f32x16& s, const u32x4* pp, u32x4* po, int kofs, int vofs, const Pre& f,
-                       auto with_qk, float& lsum) {
+                       auto with_qk, float& lsum, auto with_next, int nkofs, int nvofs, Pre& nxt) {
     constexpr bool kQK = decltype(with_qk)::value;
+    constexpr bool kNext = decltype(with_next)::value;
     f32x16 sn = f32x16{};
     bf16x8 kf[10], vf[10];
     kf[0] = f.k[0];
@@ -396,6 +399,9 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       if (i + 2 < 8) {
         if constexpr (kQK) kf[i + 2] = read_k(kofs, i + 2);
         vf[i + 2] = read_v(vofs, (i + 2) >> 2, (i + 2) & 3);
+      } else if constexpr (kNext) {
+        nxt.k[i - 6] = read_k(nkofs, i - 6);
+        nxt.v[i - 6] = read_v(nvofs, 0, i - 6);
       }
       if constexpr (kQK) sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i], qf[i], sn, 0, 0, 0);
       o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], __builtin_bit_cast(bf16x8, pp[i >> 2]), o[i & 3],
@@ -415,8 +421,8 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     slot_schedule<kQK, true>();
     slot_schedule<kQK, true>();
     slot_schedule<kQK, true>();
-    slot_schedule<kQK, false>();
-    slot_schedule<kQK, false>();
+    slot_schedule<kQK, kNext>();
+    slot_schedule<kQK, kNext>();
     return sn;
   };
   // Mask of sub-block sb0 (element e of a lane's scores is key sb0 + 8 (e / 4) + 4 half +
@@ -520,25 +526,28 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     }
 
     const int sb1 = lo + (2 * t + 1) * 32;
-    constexpr std::true_type kWithQK{};
+    constexpr std::true_type kWithQK{}, kWithNext{};
+    constexpr std::false_type kNoNext{};
+    Pre f2;   // first operands of the second step, read during the first step's last slots
     // sub-block 2t+1 (scores sc; P(2t) in pa, from scores sp)
     {
       const Pre f = prefetch(kcur, vcur, kWithQK);
       settle(sp, pa, lsum_p);
       mask(sc, sb1);
       float ls;
-      const f32x16 sn = step_main(sc, pa, pb, kcur, vcur, f, kWithQK, ls);
+      const f32x16 sn =
+          step_main(sc, pa, pb, kcur, vcur, f, kWithQK, ls, kWithNext, kcur + kSubBytes, vcur + kSubBytes, f2);
       sp = sc;
       sc = sn;
       lsum_p = ls;
     }
     // sub-block 2t+2 (P(2t+1) in pb)
     {
-      const Pre f = prefetch(kcur + kSubBytes, vcur + kSubBytes, kWithQK);
       settle(sp, pb, lsum_p);
       mask(sc, sb1 + 32);
       float ls;
-      const f32x16 sn = step_main(sc, pb, pa, kcur + kSubBytes, vcur + kSubBytes, f, kWithQK, ls);
+      const f32x16 sn =
+          step_main(sc, pb, pa, kcur + kSubBytes, vcur + kSubBytes, f2, kWithQK, ls, kNoNext, 0, 0, f2);
       sp = sc;
       sc = sn;
       lsum_p = ls;
@@ -636,11 +645,11 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     __builtin_amdgcn_s_barrier();
     const int vlast = kVBase + (t % kS) * kTileBytes;
     constexpr std::false_type kNoQK{};
-    const Pre f = prefetch(0, vlast, kNoQK);
+    Pre f = prefetch(0, vlast, kNoQK);
     settle(sp, pa, lsum_p);
     mask(sc, lo + (2 * t + 1) * 32);
     float ls;
-    step_main(sc, pa, pb, 0, vlast, f, kNoQK, ls);
+    step_main(sc, pa, pb, 0, vlast, f, kNoQK, ls, std::false_type{}, 0, 0, f);
     settle(sc, pb, ls);
     pv_acc(pb, vlast + kSubBytes);
   }
@@ -725,7 +734,7 @@ __device__ inline int upper_index(const int32_t* a, int n, int x) {
 
 // Merge of split partials: workgroup (row, y) merges heads 8y .. 8y+7 of one chunk row;
 // each thread owns 4 dims of one head.  Up to kFastPieces pieces are read in one round trip.
-constexpr int kFastPieces = 8;
+constexpr int kFastPieces = 4;
 __global__ __launch_bounds__(256) void split_reduce_kernel(uint16_t* __restrict__ out, float* __restrict__ lse,
                                                            PlanPtrs pv, int32_t num_reqs, int32_t hq) {
   const int row = blockIdx.x;
