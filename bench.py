@@ -105,6 +105,8 @@ def main():
                     help="work items the planner aims for when splitting prefixes (0 = library default)")
     ap.add_argument("--eager", action="store_true",
                     help="launch every kernel directly instead of through HIP graphs (for counter runs)")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="skip the other named workloads (config 2-5 timings in other_configs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (for counter calibration) and exit")
@@ -280,6 +282,9 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "kernel_source_sha256_16": src_hash},
     }
+    if not args.headline_only and not args.eager:
+        from paper_2604_16395_amd.benchcfg import all_configs
+        result["other_configs"] = all_configs()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(result), flush=True)

@@ -131,8 +131,13 @@ typedef struct s2l_plan_info {
   int32_t num_tiles;       /* query tiles (a split tile has one item per key-range piece)   */
   int64_t part_floats;     /* fp32 words of split partials in the workspace                 */
   int32_t key_halves;      /* wave groups per work item (1 or 2)                            */
-  int32_t reserved;
+  int32_t flags;           /* S2L_PLAN_UNIFORM: the items' key ranges are within 25% of     */
+                           /* their mean, so consecutive items (one kv head's pages) are    */
+                           /* grouped onto one XCD's L2; otherwise items run longest        */
+                           /* request first, spread over the XCDs, so the dispatcher        */
+                           /* balances them                                                 */
 } s2l_plan_info;
+#define S2L_PLAN_UNIFORM 1
 
 /* ABI version (S2L_ABI_VERSION of the built library). */
 int32_t s2l_abi_version(void);

@@ -41,7 +41,7 @@ class s2l_plan_info(ctypes.Structure):
     _fields_ = [("num_items", c_i32), ("num_split_reqs", c_i32), ("split_keys", c_i32),
                 ("num_q_heads", c_i32), ("num_kv_heads", c_i32), ("num_reqs", c_i32),
                 ("total_tokens", c_i64), ("workspace_bytes", c_i64), ("tile_cols", c_i32),
-                ("num_tiles", c_i32), ("part_floats", c_i64), ("key_halves", c_i32), ("reserved", c_i32)]
+                ("num_tiles", c_i32), ("part_floats", c_i64), ("key_halves", c_i32), ("flags", c_i32)]
 
 
 P_cache = ctypes.POINTER(s2l_kv_cache)

@@ -229,7 +229,20 @@ void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_
   info->num_tiles = (int32_t)n_tiles;
   info->part_floats = part;
   info->key_halves = o.key_halves;
-  info->reserved = 0;
+  // item key ranges: tile t of request r covers keys [0, P + i1), cut into ns pieces
+  int64_t keys_sum = 0, keys_max = 0;
+  for (int32_t r = 0; r < R; ++r) {
+    const int32_t ns = s2l::req_splits(P[r], C[r], split_keys, o.max_splits);
+    const int32_t nqt = s2l::num_qtiles(C[r], tq);
+    for (int32_t qt = 0; qt < nqt; ++qt) {
+      const int32_t i1 = std::min((qt + 1) * tq, C[r]);
+      const int64_t len = s2l::ceil_div64((int64_t)P[r] + i1, ns);
+      keys_sum += len * ns * hkv;
+      keys_max = std::max(keys_max, len);
+    }
+  }
+  const bool uniform = n_items > 0 && keys_max * n_items <= keys_sum + keys_sum / 4;
+  info->flags = uniform ? S2L_PLAN_UNIFORM : 0;
 }
 
 s2l::PlanDims plan_dims(const s2l_plan_info* p) {
@@ -290,6 +303,7 @@ s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const 
   a.dims = plan_dims(plan);
   a.tile_cols = plan->tile_cols;
   a.key_halves = plan->key_halves;
+  a.group_by_xcd = (plan->flags & S2L_PLAN_UNIFORM) != 0;
   (void)hipGetLastError();
   hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("attn_main launch", e);

@@ -13,6 +13,7 @@ namespace {
 constexpr int kPlanThreads = 256;
 constexpr int kPlanWaves = kPlanThreads / 64;
 constexpr int kLdsReqs = 1024;   // batches up to this size keep their per-request values in LDS
+constexpr int kRankReqs = kPlanThreads;   // batches up to this size are laid out longest first
 
 // Block-wide exclusive scan of N int64 values; returns the block totals in tot[].
 template <int N>
@@ -52,23 +53,50 @@ __device__ inline int upper_index(const A& a, int n, int x) {
   return lo;
 }
 
-// One pass over the requests (a contiguous segment per thread): pieces per request from the
-// host's piece length, then a block scan of items, partial floats, tiles, split requests
-// and tokens gives every offset and total.
+// Item order.  Up to kRankReqs requests are laid out longest first (by P + C, the key range
+// of their longest tile; ties by index), so that when the items take several rounds of
+// workgroups the longest start first and the dispatcher balances the tail; larger batches
+// keep request order.  Then one pass over the requests in that order (a contiguous segment
+// of slots per thread): pieces per request from the host's piece length, then a block scan
+// of items, partial floats, tiles, split requests and tokens gives every offset and total.
 __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, PlanPtrs pp) {
   __shared__ int64_t sh[5][kPlanWaves];
   __shared__ int32_t s_item_off[kLdsReqs + 1];
-  __shared__ int32_t s_tile_off[kLdsReqs], s_ns[kLdsReqs], s_p[kLdsReqs], s_c[kLdsReqs], s_cu[kLdsReqs];
+  __shared__ int32_t s_req[kLdsReqs], s_tile_off[kLdsReqs], s_ns[kLdsReqs], s_p[kLdsReqs], s_c[kLdsReqs],
+      s_cu[kLdsReqs];
   __shared__ int64_t s_part[kLdsReqs];
+  __shared__ int32_t s_key[kRankReqs], s_order[kRankReqs];
   const int R = a.num_reqs;
   const int G = a.hq / a.hkv;
   const int tq = tile_tokens(G, a.tile_cols);
   const int split_keys = a.split_keys;
+  const bool ranked = R <= kRankReqs;
+  if (ranked) {
+    const int t = threadIdx.x;
+    int key = -1;
+    if (t < R) {
+      const int P = a.prefix_lens[t], C = a.chunk_lens[t];
+      key = C > 0 ? P + C : -1;
+      s_key[t] = key;
+    }
+    __syncthreads();
+    if (t < R) {
+      int rank = 0;
+      for (int o = 0; o < R; ++o) {
+        const int ko = s_key[o];
+        rank += ko > key || (ko == key && o < t);
+      }
+      s_order[rank] = t;
+    }
+    __syncthreads();
+  }
+  auto req_at = [&](int k) { return ranked ? s_order[k] : k; };
 
   const int seg = (R + kPlanThreads - 1) / kPlanThreads;
-  const int r0 = threadIdx.x * seg, r1 = min(R, r0 + seg);
+  const int k0 = threadIdx.x * seg, k1 = min(R, k0 + seg);
   int64_t v[5] = {0, 0, 0, 0, 0}, excl[5], tot[5];
-  for (int r = r0; r < r1; ++r) {
+  for (int k = k0; k < k1; ++k) {
+    const int r = req_at(k);
     const int P = a.prefix_lens[r], C = a.chunk_lens[r];
     const int ns = req_splits(P, C, split_keys, a.max_splits);
     const int64_t tiles = (int64_t)a.hkv * num_qtiles(C, tq);
@@ -82,7 +110,8 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
   const int64_t num_items = tot[0], part_floats = tot[1], num_tiles = tot[2];
   const bool fits = num_items <= pp.cap_items && num_tiles <= pp.cap_tiles && part_floats <= pp.cap_part_floats;
   int64_t items = excl[0], part = excl[1], tiles = excl[2];
-  for (int r = r0; r < r1; ++r) {
+  for (int k = k0; k < k1; ++k) {
+    const int r = req_at(k);
     const int P = a.prefix_lens[r], C = a.chunk_lens[r];
     const int ns = req_splits(P, C, split_keys, a.max_splits);
     const int nqt = num_qtiles(C, tq);
@@ -91,14 +120,15 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     pp.c[r] = C;
     pp.cu[r] = a.cu_chunk[r];
     pp.part_off[r] = part;
-    if (R <= kLdsReqs) {
-      s_item_off[r] = (int32_t)items;
-      s_tile_off[r] = (int32_t)tiles;
-      s_ns[r] = ns;
-      s_p[r] = P;
-      s_c[r] = C;
-      s_cu[r] = a.cu_chunk[r];
-      s_part[r] = part;
+    if (R <= kLdsReqs) {   // slot-ordered copies for the item search below
+      s_item_off[k] = (int32_t)items;
+      s_req[k] = r;
+      s_tile_off[k] = (int32_t)tiles;
+      s_ns[k] = ns;
+      s_p[k] = P;
+      s_c[k] = C;
+      s_cu[k] = a.cu_chunk[r];
+      s_part[k] = part;
     }
     items += (int64_t)a.hkv * nqt * ns;
     part += req_part_floats(ns, C, a.hq);
@@ -132,10 +162,11 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     int r, tile0, P, C, ns, row0, off;
     int64_t part_off;
     if (R <= kLdsReqs) {
-      r = upper_index(s_item_off, R, w);
-      tile0 = s_tile_off[r];
-      P = s_p[r], C = s_c[r], ns = s_ns[r], row0 = s_cu[r], off = s_item_off[r], part_off = s_part[r];
-    } else {
+      const int k = upper_index(s_item_off, R, w);
+      r = s_req[k];
+      tile0 = s_tile_off[k];
+      P = s_p[k], C = s_c[k], ns = s_ns[k], row0 = s_cu[k], off = s_item_off[k], part_off = s_part[k];
+    } else {   // request order (no ranking above kRankReqs requests), offsets in global memory
       r = upper_index(pp.item_off, R, w);
       tile0 = 0;
       for (int k = 0; k < r; ++k) tile0 += a.hkv * num_qtiles(a.chunk_lens[k], tq);

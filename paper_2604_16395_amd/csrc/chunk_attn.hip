@@ -157,7 +157,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out, float* __restrict__ lse,
     const void* __restrict__ kpool, const void* __restrict__ vpool, const float* __restrict__ kscale,
     const float* __restrict__ vscale, const int32_t* __restrict__ block_tables, int32_t max_pages, int32_t hq,
-    int32_t hkv, float scale_log2, PlanPtrs pv) {
+    int32_t hkv, float scale_log2, PlanPtrs pv, int32_t group_by_xcd) {
   using RingT = Ring<kFp8, kColWaves, kHalves>;
   constexpr int kWaves = kColWaves * kHalves;
   constexpr int kS = RingT::kStages;
@@ -173,8 +173,11 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   __shared__ __attribute__((aligned(1024))) uint8_t smem[RingT::kBytes];
   __shared__ __attribute__((aligned(256))) int32_t s_pages[kWaves][2][64];   // next page windows
 
-  // the item (one scalar load) and the device plan's item count, fetched together
-  const int w_item = xcd_logical(blockIdx.x, gridDim.x);
+  // the item (one scalar load) and the device plan's item count, fetched together.  When
+  // the items cost about the same, consecutive items (one kv head's pages) go to one XCD's
+  // L2; otherwise workgroups take items in plan order (longest request first), which the
+  // round-robin dispatch spreads evenly over the XCDs.
+  const int w_item = group_by_xcd ? xcd_logical(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const ItemRec it = pv.items[w_item];
   const int W = pv.hdr->num_items;
   if (w_item >= W) return;   // the device plan did not fit this launch (nothing planned)
@@ -797,7 +800,7 @@ void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
   attn_main_kernel<kFp8, kColWaves, kHalves><<<(unsigned)a.dims.num_items, kColWaves * kHalves * 64, 0, stream>>>(
       static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
       a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, a.softmax_scale * kLog2e,
-      plan_ptrs(a.workspace, a.dims));
+      plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0);
 }
 
 template <bool kFp8>

@@ -49,6 +49,7 @@ struct AttnLaunch {
   PlanDims dims;            // host copy of the plan's sizes (grid = dims.num_items)
   int32_t tile_cols;        // 128 or 256 (host copy of the plan's tile width)
   int32_t key_halves;       // 1 or 2 wave groups per item, each on half of its key range
+  bool group_by_xcd;        // items of near-equal cost: consecutive items onto one XCD
 };
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream);
 

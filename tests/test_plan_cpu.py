@@ -130,3 +130,15 @@ def test_empty_and_degenerate_batches():
     assert info.num_items == 0
     info, items = s2l_plan_host([0], [1], 8, 8, plan_opts(target_items=8), with_items=True)
     assert info.num_items == 8 and set(map(tuple, items[:, 2:6])) == {(0, 1, 0, 1)}
+
+
+def test_uniform_items_flag():
+    # one request: every item's key range within a few percent of the mean
+    info, _ = s2l_plan_host([8192], [512], 32, 8, num_cus=256)
+    assert info.flags & 1
+    info, _ = s2l_plan_host([131072], [2048], 64, 8, num_cus=256)
+    assert info.flags & 1
+    # the mixed 64-request batch: ranges from a handful of keys to 34K
+    P, C, _ = workloads.config4_lengths()
+    info, _ = s2l_plan_host(P, C, 32, 8, num_cus=256)
+    assert not (info.flags & 1)
