@@ -1,4 +1,5 @@
-"""ctypes declarations of the C ABI in include/s2l.h and the loader of libs2l.so.
+"""ctypes declarations of the C ABI in include/s2l.h and include/s2l_sched.h, and the
+loader of libs2l.so.
 
 Loading fails loudly (S2LLibraryMissing) when the built library is absent: there is no
 fallback implementation of any entry point.
@@ -44,6 +45,36 @@ class s2l_plan_info(ctypes.Structure):
                 ("num_tiles", c_i32), ("part_floats", c_i64), ("key_halves", c_i32), ("flags", c_i32)]
 
 
+class s2l_sched_config(ctypes.Structure):
+    _fields_ = [("policy", c_i32), ("num_gpu_blocks", c_i32), ("num_cpu_blocks", c_i32),
+                ("token_budget", c_i32), ("max_blocks_per_req", c_i32), ("table_pad", c_i32),
+                ("num_recompute_points", c_i32), ("reserved", c_i32),
+                ("recompute_tokens", ctypes.POINTER(ctypes.c_double)),
+                ("recompute_seconds", ctypes.POINTER(ctypes.c_double)),
+                ("swap_fixed_seconds", ctypes.c_double), ("swap_seconds_per_block", ctypes.c_double)]
+
+
+class s2l_sched_step_out(ctypes.Structure):
+    _fields_ = [("req_ids", c_vp), ("prefix_lens", c_vp), ("chunk_lens", c_vp), ("block_tables", c_vp),
+                ("event_ids", c_vp), ("event_kinds", c_vp), ("swap_out", c_vp), ("swap_in", c_vp),
+                ("cap_reqs", c_i32), ("cap_swap", c_i32), ("num_reqs", c_i32), ("num_events", c_i32),
+                ("num_swap_out", c_i32), ("num_swap_in", c_i32), ("total_tokens", c_i32),
+                ("reserved", c_i32), ("order_ns", c_i64), ("step_ns", c_i64)]
+
+
+class s2l_sched_req_info(ctypes.Structure):
+    _fields_ = [("state", c_i32), ("num_tokens", c_i32), ("num_computed_tokens", c_i32),
+                ("input_complete", c_i32), ("total_tokens_invalidated", c_i64),
+                ("num_preempt_swap", c_i32), ("num_preempt_recompute", c_i32),
+                ("num_gpu_blocks", c_i32), ("num_cpu_blocks", c_i32),
+                ("arrival_time", ctypes.c_double), ("last_chunk_arrival_time", ctypes.c_double)]
+
+
+class s2l_sched_stats(ctypes.Structure):
+    _fields_ = [("num_unfinished", c_i32), ("free_gpu_blocks", c_i32), ("free_cpu_blocks", c_i32),
+                ("reserved", c_i32)]
+
+
 P_cache = ctypes.POINTER(s2l_kv_cache)
 P_batch = ctypes.POINTER(s2l_batch)
 P_opts = ctypes.POINTER(s2l_plan_opts)
@@ -63,6 +94,17 @@ SIGNATURES = {
                               c_vp, ctypes.c_size_t, c_vp]),
     "s2l_split_reduce": (c_i32, [P_batch, c_i32, c_vp, c_vp, P_info, c_vp, ctypes.c_size_t, c_vp]),
     "s2l_plan_host": (c_i32, [c_i32, P_i32, P_i32, c_i32, c_i32, P_opts, c_i32, P_info, P_i32, c_i64]),
+    # include/s2l_sched.h
+    "s2l_lcp_len": (c_i32, [P_i32, c_i32, P_i32, c_i32]),
+    "s2l_sched_create": (c_i32, [ctypes.POINTER(s2l_sched_config), ctypes.POINTER(c_vp)]),
+    "s2l_sched_destroy": (None, [c_vp]),
+    "s2l_sched_new_stream": (c_i32, [c_vp, c_i64, P_i32, c_i32, c_i32, ctypes.c_double]),
+    "s2l_sched_append": (c_i32, [c_vp, c_i64, P_i32, c_i32, c_i32, ctypes.c_double]),
+    "s2l_sched_update": (c_i32, [c_vp, c_i64, P_i32, c_i32, c_i32, ctypes.c_double, P_i32]),
+    "s2l_sched_step": (c_i32, [c_vp, ctypes.POINTER(s2l_sched_step_out)]),
+    "s2l_sched_priority_order": (c_i32, [c_vp, ctypes.POINTER(c_i64), c_i32, P_i32, ctypes.POINTER(c_i64)]),
+    "s2l_sched_request": (c_i32, [c_vp, c_i64, ctypes.POINTER(s2l_sched_req_info), P_i32, P_i32]),
+    "s2l_sched_stats_get": (c_i32, [c_vp, ctypes.POINTER(s2l_sched_stats)]),
 }
 
 

@@ -222,6 +222,40 @@ def cfg5(stream, gen):
             "work_items": plan.num_items, "tile_cols": plan.tile_cols}
 
 
+def scheduler_latency(seed=2024, sizes=(50, 500), calls=2000):
+    """Host latency of the scheduler's policy ordering (the sort) and of a whole two-phase
+    step with `n` unfinished requests, per policy: median and P99 over `calls` calls.
+    Requests come from the synthetic crawler/ANNS streams (all arrived, some chunks in)."""
+    from . import sched as S
+    from workloads.streams import stream_events
+    out = {}
+    for n in sizes:
+        events = stream_events(seed, n, mode="mixed", rate=1e4, token_scale=0.25, max_tokens=8192)
+        horizon = events[len(events) // 2][0]
+        for name, pol in S.POLICIES.items():
+            s = S.Scheduler(pol, num_gpu_blocks=65536, num_cpu_blocks=65536, token_budget=8192,
+                            max_blocks_per_req=512, recompute=([1024.0, 131072.0], [0.02, 2.0]),
+                            swap=(0.0005, 0.00004))
+            for t, kind, rid, ids, complete in events:
+                if t > horizon:
+                    break
+                getattr(s, "new_stream" if kind == "new" else kind)(rid, ids, complete, t)
+            s.step()
+            order = np.array([s.priority_order()[1] for _ in range(calls)], dtype=np.float64)
+            live = s.stats().num_unfinished
+            steps = []
+            for _ in range(20):
+                steps.append(s.step().step_ns)
+            out[f"{name}_n{n}"] = {
+                "unfinished": live,
+                "order_us_p50": round(float(np.median(order)) / 1e3, 3),
+                "order_us_p99": round(float(np.percentile(order, 99)) / 1e3, 3),
+                "step_us_p50": round(float(np.median(steps)) / 1e3, 3)}
+    out["paper_sort_us_at_50"] = {"FCFS": "15-16", "LCAS": "15-16", "MCPS": "12-13"}
+    out["paper_p99_us_at_500"] = "< 165"
+    return out
+
+
 def all_configs(seed=2024):
     """{config name: result or error string}; each config is measured independently."""
     stream = torch.cuda.Stream()
@@ -235,4 +269,8 @@ def all_configs(seed=2024):
             res[name] = {"error": f"{type(e).__name__}: {e}"}
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
+    try:
+        res["scheduler"] = scheduler_latency(seed)
+    except Exception as e:
+        res["scheduler"] = {"error": f"{type(e).__name__}: {e}"}
     return res

@@ -13,10 +13,13 @@
 
 #include "launch.h"
 #include "plan_rules.h"
+#include "status.h"
 
 namespace {
-
 thread_local std::string g_err;
+}  // namespace
+
+namespace s2l {
 
 s2l_status fail(s2l_status st, const char* fmt, ...) {
   char buf[512];
@@ -32,6 +35,13 @@ s2l_status ok() {
   g_err.clear();
   return S2L_OK;
 }
+
+}  // namespace s2l
+
+namespace {
+
+using s2l::fail;
+using s2l::ok;
 
 s2l_status hip_fail(const char* what, hipError_t e) {
   return fail(S2L_EHIP, "%s: %s", what, hipGetErrorString(e));

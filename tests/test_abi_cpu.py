@@ -5,6 +5,7 @@ Every call here fails host-side validation, so no kernel is ever enqueued (the d
 pointers below are placeholders that are never dereferenced).
 """
 import ctypes
+import glob
 import os
 import re
 
@@ -18,9 +19,11 @@ FAKE = 0x10000  # placeholder device address, never dereferenced (validation fai
 
 
 def header_functions():
-    text = open(os.path.join(ROOT, "include", "s2l.h")).read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return set(re.findall(r"\b(s2l_[a-z0-9_]+)\s*\(", text))
+    names = set()
+    for h in sorted(glob.glob(os.path.join(ROOT, "include", "*.h"))):
+        text = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(s2l_[a-z0-9_]+)\s*\(", text))
+    return names
 
 
 def test_library_exports_every_declared_function():
