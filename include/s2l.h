@@ -169,6 +169,26 @@ s2l_status s2l_kv_gather(const s2l_kv_cache* cache, const s2l_batch* batch, int3
                          const int32_t* cu_out, void* k_out, void* v_out, void* stream);
 
 /*
+ * Swap-out and swap-in of KV pages (Sec. 4.3: a preempted request's blocks move to CPU
+ * memory and come back when it resumes; Sec. 4.2: blocks past an update's LCP are simply
+ * dropped).  One layer's pages move between the device pools of `cache` and two pinned
+ * host pools host_k, host_v laid out like them, [num_host_pages][num_kv_heads][16][128]
+ * of the cache's element type (bf16 or fp8 codes: pages move as bytes, bit-exact).
+ *   pairs: DEVICE int32 [n][2]; swap_out copies device page pairs[i][0] to host page
+ *          pairs[i][1]; swap_in copies host page pairs[i][0] to device page pairs[i][1]
+ *          (the scheduler's swap_out / swap_in lists have exactly these forms).  A pair
+ *          whose page ids fall outside [0, num_pages) or [0, num_host_pages) is skipped.
+ *   host_k, host_v: pinned host memory (hipHostMalloc, or torch pin_memory) that the GPU
+ *          reads or writes directly over the host link; anything else is S2L_EINVAL.
+ *          The caller keeps them alive until the stream has passed the copy.
+ * Pages of one call must be distinct on the destination side.  Asynchronous on `stream`.
+ */
+s2l_status s2l_kv_swap_out(const s2l_kv_cache* cache, const int32_t* pairs, int32_t n, void* host_k,
+                           void* host_v, int32_t num_host_pages, void* stream);
+s2l_status s2l_kv_swap_in(const s2l_kv_cache* cache, const int32_t* pairs, int32_t n, const void* host_k,
+                          const void* host_v, int32_t num_host_pages, void* stream);
+
+/*
  * Workspace bytes that s2l_attn_plan and the attention calls need for this batch (host
  * computation from the host length copies; opts as for s2l_attn_plan).
  */

@@ -23,7 +23,7 @@ from ._lib import (S2L_KV_BF16, S2L_KV_FP8_E4M3, S2LError, S2LLibraryMissing, s2
                    s2l_plan_opts)
 
 __all__ = ["PagedKVCache", "Batch", "plan_opts", "S2LError", "S2LLibraryMissing",
-           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_attn_workspace_bytes",
+           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in", "s2l_attn_workspace_bytes",
            "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_attn_main", "s2l_split_reduce",
            "s2l_plan_host", "library_path"]
 
@@ -140,6 +140,29 @@ def s2l_kv_append(cache, batch, k_new, v_new, stream=None):
     _check(v_new, torch.bfloat16, "v_new")
     cc, bc = cache.c(), batch.c()
     _lib.call("s2l_kv_append", ctypes.byref(cc), ctypes.byref(bc), _ptr(k_new), _ptr(v_new), _stream(stream))
+
+
+def _swap(name, cache, pairs, host_k, host_v, stream):
+    _check(pairs, torch.int32, "pairs")
+    if pairs.dim() != 2 or pairs.shape[1] != 2 or not pairs.is_cuda:
+        raise ValueError("pairs must be a device int32 tensor [n][2]")
+    if host_k.is_cuda or host_v.is_cuda or host_k.dtype != cache.k_pages.dtype or host_v.dtype != host_k.dtype:
+        raise ValueError("host pools must be host tensors of the cache's element type")
+    if not (host_k.is_contiguous() and host_v.is_contiguous()) or host_k.shape != host_v.shape:
+        raise ValueError("host pools must be contiguous and of one shape")
+    cc = cache.c()
+    _lib.call(name, ctypes.byref(cc), _ptr(pairs), pairs.shape[0], _ptr(host_k), _ptr(host_v),
+              host_k.shape[0], _stream(stream))
+
+
+def s2l_kv_swap_out(cache, pairs, host_k, host_v, stream=None):
+    """Device pages pairs[i][0] -> pinned host pages pairs[i][1] (K and V)."""
+    _swap("s2l_kv_swap_out", cache, pairs, host_k, host_v, stream)
+
+
+def s2l_kv_swap_in(cache, pairs, host_k, host_v, stream=None):
+    """Pinned host pages pairs[i][0] -> device pages pairs[i][1] (K and V)."""
+    _swap("s2l_kv_swap_in", cache, pairs, host_k, host_v, stream)
 
 
 def s2l_kv_gather(cache, batch, include_chunk, cu_out, k_out, v_out, stream=None):

@@ -351,6 +351,51 @@ s2l_status s2l_kv_append(const s2l_kv_cache* cache, const s2l_batch* batch, cons
   return ok();
 }
 
+// Swap between the device page pools and pinned host pools of the same layout.
+static s2l_status kv_swap(const char* what, const s2l_kv_cache* cache, const int32_t* pairs, int32_t n,
+                          const void* host_k, const void* host_v, int32_t num_host_pages, bool to_host,
+                          void* stream) {
+  s2l_status st;
+  if ((st = check_cache(cache, nullptr)) != S2L_OK) return st;
+  if (n < 0) return fail(S2L_EINVAL, "%s: negative pair count %d", what, n);
+  if (n == 0) return ok();
+  if (n > 65535 * 1024) return fail(S2L_EINVAL, "%s: %d pairs exceed one launch", what, n);
+  if (!pairs) return fail(S2L_EINVAL, "%s: pairs is NULL", what);
+  if (num_host_pages <= 0) return fail(S2L_EINVAL, "%s: num_host_pages must be > 0", what);
+  void* dev_view[2] = {nullptr, nullptr};
+  const void* host[2] = {host_k, host_v};
+  for (int i = 0; i < 2; ++i) {
+    if (!host[i]) return fail(S2L_EINVAL, "%s: host pool is NULL", what);
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, host[i]);
+    (void)hipGetLastError();
+    if (e != hipSuccess || attr.type != hipMemoryTypeHost || !attr.devicePointer)
+      return fail(S2L_EINVAL, "%s: host pool %c is not pinned host memory (allocate it with hipHostMalloc)",
+                  what, i ? 'v' : 'k');
+    dev_view[i] = attr.devicePointer;
+  }
+  const int64_t page_bytes = (int64_t)cache->num_kv_heads * s2l::kPageSize * s2l::kHeadDim *
+                             (cache->dtype == S2L_KV_FP8_E4M3 ? 1 : 2);
+  (void)hipGetLastError();
+  hipError_t e = to_host
+      ? s2l::launch_kv_page_copy(cache->k_pages, cache->v_pages, dev_view[0], dev_view[1], pairs, n,
+                                 cache->num_pages, num_host_pages, page_bytes, static_cast<hipStream_t>(stream))
+      : s2l::launch_kv_page_copy(dev_view[0], dev_view[1], cache->k_pages, cache->v_pages, pairs, n,
+                                 num_host_pages, cache->num_pages, page_bytes, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(what, e);
+  return ok();
+}
+
+s2l_status s2l_kv_swap_out(const s2l_kv_cache* cache, const int32_t* pairs, int32_t n, void* host_k, void* host_v,
+                           int32_t num_host_pages, void* stream) {
+  return kv_swap("kv_swap_out", cache, pairs, n, host_k, host_v, num_host_pages, true, stream);
+}
+
+s2l_status s2l_kv_swap_in(const s2l_kv_cache* cache, const int32_t* pairs, int32_t n, const void* host_k,
+                          const void* host_v, int32_t num_host_pages, void* stream) {
+  return kv_swap("kv_swap_in", cache, pairs, n, host_k, host_v, num_host_pages, false, stream);
+}
+
 s2l_status s2l_kv_gather(const s2l_kv_cache* cache, const s2l_batch* batch, int32_t include_chunk,
                          const int32_t* cu_out, void* k_out, void* v_out, void* stream) {
   s2l_status st;

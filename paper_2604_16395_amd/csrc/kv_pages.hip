@@ -1,4 +1,4 @@
-// Page append (scatter) and gather kernels for the paged KV cache.
+// Page append (scatter), gather and page-copy (swap) kernels for the paged KV cache.
 //
 // Paging (Stream2LLM Sec. 2.2): token p of a request lives in logical page p / 16, slot
 // p % 16; the block table maps logical pages to physical ones.  Append (Sec. 4.2 /
@@ -82,7 +82,43 @@ __global__ __launch_bounds__(256) void kv_gather_kernel(
   }
 }
 
+// Page copy between two pools of the same layout (swap-out: device pool -> pinned host
+// pool; swap-in: the reverse).  Workgroup (i, pool) copies pair i's whole page of K
+// (pool 0) or V (pool 1): page_bytes contiguous bytes, as 16-byte units, eight loads in
+// flight per thread before their stores (host memory is far: latency needs depth).  A
+// pair with a page id outside its pool is skipped.
+__global__ __launch_bounds__(256) void kv_page_copy_kernel(
+    const char* __restrict__ src_k, const char* __restrict__ src_v, char* __restrict__ dst_k,
+    char* __restrict__ dst_v, const int32_t* __restrict__ pairs, int32_t num_src, int32_t num_dst,
+    int64_t page_bytes) {
+  const int32_t sp = pairs[2 * blockIdx.x], dp = pairs[2 * blockIdx.x + 1];
+  if (sp < 0 || sp >= num_src || dp < 0 || dp >= num_dst) return;
+  const u32x4* src = reinterpret_cast<const u32x4*>((blockIdx.y ? src_v : src_k) + sp * page_bytes);
+  u32x4* dst = reinterpret_cast<u32x4*>((blockIdx.y ? dst_v : dst_k) + dp * page_bytes);
+  const int units = (int)(page_bytes / 16);
+  constexpr int kDepth = 8;
+  for (int u0 = threadIdx.x; u0 < units; u0 += 256 * kDepth) {
+    u32x4 x[kDepth];
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j)
+      if (u0 + j * 256 < units) x[j] = src[u0 + j * 256];
+#pragma unroll
+    for (int j = 0; j < kDepth; ++j)
+      if (u0 + j * 256 < units) dst[u0 + j * 256] = x[j];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_kv_page_copy(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
+                               const int32_t* pairs, int32_t n, int32_t num_src, int32_t num_dst,
+                               int64_t page_bytes, hipStream_t stream) {
+  if (n == 0) return hipSuccess;
+  kv_page_copy_kernel<<<dim3(n, 2), 256, 0, stream>>>(
+      static_cast<const char*>(src_k), static_cast<const char*>(src_v), static_cast<char*>(dst_k),
+      static_cast<char*>(dst_v), pairs, num_src, num_dst, page_bytes);
+  return hipGetLastError();
+}
 
 hipError_t launch_kv_append(const KvLaunch& a, const void* knew, const void* vnew, int32_t max_pages_touched,
                             hipStream_t stream) {

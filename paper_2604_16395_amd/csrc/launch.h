@@ -26,6 +26,12 @@ hipError_t launch_kv_append(const KvLaunch& a, const void* knew, const void* vne
                             hipStream_t stream);
 hipError_t launch_kv_gather(const KvLaunch& a, int32_t include_chunk, const int32_t* cu_out, void* kout,
                             void* vout, int32_t max_pages_read, hipStream_t stream);
+// Copies whole (page, all kv heads) runs of K and V from pages pairs[i][0] of the source
+// pools to pages pairs[i][1] of the destination pools (either side may be pinned host
+// memory); pairs is a device array; pairs outside [0, num_src) x [0, num_dst) are skipped.
+hipError_t launch_kv_page_copy(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
+                               const int32_t* pairs, int32_t n, int32_t num_src, int32_t num_dst,
+                               int64_t page_bytes, hipStream_t stream);
 
 struct PlanLaunch {
   const int32_t* prefix_lens;

@@ -63,6 +63,7 @@ class Scheduler:
         h = ctypes.c_void_p()
         _lib.call("s2l_sched_create", ctypes.byref(cfg), ctypes.byref(h))
         self._h = h
+        self._destroy = _lib.lib().s2l_sched_destroy
         self.max_blocks = max_blocks_per_req
         self.num_gpu_blocks = num_gpu_blocks
         self._cap = 0
@@ -71,7 +72,7 @@ class Scheduler:
     def __del__(self):
         h = getattr(self, "_h", None)
         if h is not None and h.value:
-            _lib.lib().s2l_sched_destroy(h)
+            self._destroy(h)
             self._h = None
 
     def _grow(self, cap):

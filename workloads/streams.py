@@ -62,3 +62,38 @@ def stream_events(seed, num_reqs, mode="append", rate=2.0, token_scale=1.0, max_
                 events.append((t + float(times[j - 1]), "update", rid, cur, j == k - 1))
     events.sort(key=lambda e: (e[0], e[2]))
     return events
+
+
+def prefix_hashes(ids):
+    """64-bit FNV-1a style rolling hash of every prefix ids[0..p], p = 0 .. len-1."""
+    out = np.zeros(len(ids), dtype=np.uint64)
+    h = 1469598103934665603
+    for p, t in enumerate(ids):
+        h = ((h ^ (int(t) + 1)) * 1099511628211) & 0xFFFFFFFFFFFFFFFF
+        out[p] = h
+    return out
+
+
+def prefix_rows(ids, start, end, hq, hkv, seed, sigma=0.5, head_dim=128, memo=None):
+    """bf16 bit rows (Q [n][hq][D], K and V [n][hkv][D]) of positions [start, end) of the
+    token sequence `ids`.  Row p is drawn from a generator seeded by (seed, hash of
+    ids[0..p]): sequences that share a prefix share exactly those rows, as a model's
+    activations would.  `memo` (a dict) keeps rows by prefix hash across calls."""
+    from . import bf16_bits
+    hs = prefix_hashes(ids[:end])
+    n = end - start
+    q = np.empty((n, hq, head_dim), np.uint16)
+    k = np.empty((n, hkv, head_dim), np.uint16)
+    v = np.empty((n, hkv, head_dim), np.uint16)
+    for i, p in enumerate(range(start, end)):
+        h = int(hs[p])
+        got = memo.get(h) if memo is not None else None
+        if got is None:
+            rng = np.random.default_rng([seed, h])
+            got = (bf16_bits(rng.standard_normal((hq, head_dim), dtype=np.float32) * sigma),
+                   bf16_bits(rng.standard_normal((hkv, head_dim), dtype=np.float32) * sigma),
+                   bf16_bits(rng.standard_normal((hkv, head_dim), dtype=np.float32) * sigma))
+            if memo is not None:
+                memo[h] = got
+        q[i], k[i], v[i] = got
+    return q, k, v
