@@ -270,6 +270,17 @@ def all_configs(seed=2024):
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
     try:
+        from . import costmodel
+        swap = costmodel.measure_swap()
+        rec = costmodel.measure_recompute(token_counts=(1024, 16384, 131072))
+        res["cost_model"] = {
+            "swap_kernel_gbs": {"out": round(swap["kernel_out_gbs"], 1), "in": round(swap["kernel_in_gbs"], 1)},
+            "memcpy_gbs": {"d2h": round(swap["memcpy_d2h_gbs"], 1), "h2d": round(swap["memcpy_h2d_gbs"], 1)},
+            "swap_fit_round_trip_s": swap["fit_round_trip_s"],
+            "compare": costmodel.crossover(swap, rec)}
+    except Exception as e:
+        res["cost_model"] = {"error": f"{type(e).__name__}: {e}"}
+    try:
         res["scheduler"] = scheduler_latency(seed)
     except Exception as e:
         res["scheduler"] = {"error": f"{type(e).__name__}: {e}"}

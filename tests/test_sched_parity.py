@@ -143,3 +143,20 @@ def test_scheduler_rejects_bad_configs():
         L.Scheduler(9, 8, 0, 8, 4, REC, SWAP)
     with pytest.raises(_lib.S2LError):
         L.Scheduler(0, 8, 0, 8, 4, ([10.0, 5.0], [1.0, 2.0]), SWAP)
+
+
+def test_measured_cost_model_drives_the_scheduler():
+    from paper_2604_16395_amd import costmodel
+    rec, swap = costmodel.load()
+    assert len(rec[0]) >= 2 and all(b > a for a, b in zip(rec[0], rec[0][1:]))
+    assert all(t > 0 for t in rec[1]) and swap[1] > 0
+    s = L.Scheduler(L.POLICY_MCPS, 4, 8, 1000, 8, rec, swap)
+    o = O.Scheduler(L.POLICY_MCPS, 4, 8, 1000, 8, rec[0], rec[1], swap[0], swap[1])
+    for x in (s, o):
+        x.new_stream(1, list(range(48)), False, 0.0)
+        x.step()
+        x.new_stream(2, list(range(100, 164)), True, 1.0)
+    a, b = s.step(), o.step()
+    _compare_step(b, a, "cost model")
+    # on this GPU moving 3 blocks over the host link beats recomputing 48 tokens
+    assert a.events == [(1, L.EV_PREEMPT_SWAP)]
