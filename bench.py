@@ -282,6 +282,11 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "kernel_source_sha256_16": src_hash},
     }
+    if not args.eager:
+        from paper_2604_16395_amd.benchcfg import measured_ceilings
+        ceil = measured_ceilings()
+        ceil["attn_frac_of_measured_mfma"] = round(achieved / ceil["mfma_bf16_tflops"], 4)
+        result["measured_ceilings"] = ceil
     if not args.headline_only and not args.eager:
         from paper_2604_16395_amd.benchcfg import all_configs
         result["other_configs"] = all_configs()

@@ -266,6 +266,20 @@ s2l_status s2l_plan_host(int32_t num_reqs, const int32_t* prefix_lens_host, cons
                          int32_t num_q_heads, int32_t num_kv_heads, const s2l_plan_opts* opts,
                          int32_t num_cus, s2l_plan_info* info, int32_t* items_out, int64_t item_capacity);
 
+/*
+ * Measurement support (not part of the attention path): ceilings measured on the GPU at
+ * hand, for reporting the kernels against.
+ *   s2l_calib_stream_read: one streaming read of `bytes` (device, a multiple of 16, > 0)
+ *     by `grid` workgroups of 256 threads; each thread writes one word of `sink` (device,
+ *     grid * 256 uint32).  Bytes read / kernel time = reachable HBM read bandwidth.
+ *   s2l_calib_mfma_bf16: `iters` steps of four independent 32x32x16 bf16 MFMA chains per
+ *     wave, `grid` workgroups of four waves, no memory traffic; `sink` (device, grid * 256
+ *     floats) receives one result per thread; *flops_out = the MFMA flops it issues.
+ * Both are asynchronous on `stream`; time them with events.
+ */
+s2l_status s2l_calib_stream_read(const void* buf, size_t bytes, uint32_t* sink, int32_t grid, void* stream);
+s2l_status s2l_calib_mfma_bf16(int64_t iters, float* sink, int32_t grid, int64_t* flops_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -23,7 +23,8 @@ from ._lib import (S2L_KV_BF16, S2L_KV_FP8_E4M3, S2LError, S2LLibraryMissing, s2
                    s2l_plan_opts)
 
 __all__ = ["PagedKVCache", "Batch", "plan_opts", "S2LError", "S2LLibraryMissing",
-           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in", "s2l_attn_workspace_bytes",
+           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in",
+           "s2l_calib_stream_read", "s2l_calib_mfma_bf16", "s2l_attn_workspace_bytes",
            "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_attn_main", "s2l_split_reduce",
            "s2l_plan_host", "library_path"]
 
@@ -163,6 +164,19 @@ def s2l_kv_swap_out(cache, pairs, host_k, host_v, stream=None):
 def s2l_kv_swap_in(cache, pairs, host_k, host_v, stream=None):
     """Pinned host pages pairs[i][0] -> device pages pairs[i][1] (K and V)."""
     _swap("s2l_kv_swap_in", cache, pairs, host_k, host_v, stream)
+
+
+def s2l_calib_stream_read(buf, sink, grid, stream=None):
+    """One streaming read of the device tensor `buf` (measurement support)."""
+    _lib.call("s2l_calib_stream_read", _ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), int(grid),
+              _stream(stream))
+
+
+def s2l_calib_mfma_bf16(iters, sink, grid, stream=None):
+    """A register-only bf16 MFMA loop (measurement support); returns its flop count."""
+    flops = ctypes.c_int64()
+    _lib.call("s2l_calib_mfma_bf16", int(iters), _ptr(sink), int(grid), ctypes.byref(flops), _stream(stream))
+    return flops.value
 
 
 def s2l_kv_gather(cache, batch, include_chunk, cu_out, k_out, v_out, stream=None):

@@ -96,6 +96,8 @@ SIGNATURES = {
                               c_vp, ctypes.c_size_t, c_vp]),
     "s2l_split_reduce": (c_i32, [P_batch, c_i32, c_vp, c_vp, P_info, c_vp, ctypes.c_size_t, c_vp]),
     "s2l_plan_host": (c_i32, [c_i32, P_i32, P_i32, c_i32, c_i32, P_opts, c_i32, P_info, P_i32, c_i64]),
+    "s2l_calib_stream_read": (c_i32, [c_vp, ctypes.c_size_t, c_vp, c_i32, c_vp]),
+    "s2l_calib_mfma_bf16": (c_i32, [c_i64, c_vp, c_i32, ctypes.POINTER(c_i64), c_vp]),
     # include/s2l_sched.h
     "s2l_lcp_len": (c_i32, [P_i32, c_i32, P_i32, c_i32]),
     "s2l_sched_create": (c_i32, [ctypes.POINTER(s2l_sched_config), ctypes.POINTER(c_vp)]),

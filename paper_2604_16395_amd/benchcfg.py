@@ -205,6 +205,16 @@ def cfg4(stream, gen):
                                 "kv_gbs": round(d.kv_bytes() / dus / 1e3, 1),
                                 "pct_hbm_peak": round(100 * d.kv_bytes() / dus / 1e3 / PEAK_HBM_GBS, 1),
                                 "work_items": dplan.num_items, "tile_cols": dplan.tile_cols}
+        del d
+        torch.cuda.empty_cache()
+        # 64 decode rows over 32K prefixes each (a steady decode batch)
+        P64, C64 = np.full(64, 32768, np.int32), np.ones(64, np.int32)
+        pool64 = int(((P64 + C64 + 15) // 16).sum() + 16)
+        d = Layer(P64, C64, 32, 8, pool64, tables_for(P64, C64, pool64, rng), gen, copies=2)
+        _, dus, dplan = measure_step(d, stream, 2)
+        res["decode_64x32k"] = {"attn_us": round(dus, 2), "kv_gbs": round(d.kv_bytes() / dus / 1e3, 1),
+                                "pct_hbm_peak": round(100 * d.kv_bytes() / dus / 1e3 / PEAK_HBM_GBS, 1),
+                                "work_items": dplan.num_items, "tile_cols": dplan.tile_cols}
     return res
 
 
@@ -254,6 +264,33 @@ def scheduler_latency(seed=2024, sizes=(50, 500), calls=2000):
     out["paper_sort_us_at_50"] = {"FCFS": "15-16", "LCAS": "15-16", "MCPS": "12-13"}
     out["paper_p99_us_at_500"] = "< 165"
     return out
+
+
+def measured_ceilings(stream=None):
+    """HBM read bandwidth of a plain streaming kernel (best of several grid sizes) and the
+    bf16 MFMA rate of a register-only loop, both measured here with the library's
+    calibration kernels and HIP events."""
+    stream = stream or torch.cuda.Stream()
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    buf = torch.ones(1 << 30, dtype=torch.float32, device="cuda")          # 4 GiB
+    best = 0.0
+    for per_cu in (2, 8, 16):
+        sink = torch.empty(cus * per_cu * 256, dtype=torch.int32, device="cuda")
+        ms = timed_graph(lambda: s2l.s2l_calib_stream_read(buf, sink, cus * per_cu, stream), stream, reps=5)
+        best = max(best, buf.numel() * 4 / ms / 1e6)
+    del buf
+    sink = torch.empty(cus * 2 * 256, dtype=torch.float32, device="cuda")
+    flops = 0
+
+    def loop():
+        nonlocal flops
+        flops = s2l.s2l_calib_mfma_bf16(20000, sink, cus * 2, stream)
+
+    ms = timed_graph(loop, stream, reps=3)
+    torch.cuda.empty_cache()
+    return {"hbm_read_gbs": round(best, 1), "mfma_bf16_tflops": round(flops / ms / 1e9, 1),
+            "how": "streaming-read kernel over 4 GiB (best of 2, 8, 16 workgroups per CU); "
+                   "register-only loop of 32x32x16 bf16 MFMAs, 8 waves per CU"}
 
 
 def all_configs(seed=2024):

@@ -51,12 +51,16 @@ struct Resolved {
   int32_t target_items, min_split_keys, max_splits, tile_cols, key_halves;
 };
 
-// Automatic tile width: 256-column tiles (8-wave workgroups sharing each K/V tile, with a
-// four-stage copy ring; the fastest layout measured on the 8K-prefix, 512-token step)
-// unless they would be less than half full on average, as in batches of mostly decode-like
-// rows (C * G well below 256 columns per request and kv head); then 128.
+// Automatic tile width: 16-column decode tiles when every request fits one (C * G <= 16:
+// decode-shaped batches, bound by reading the keys); otherwise 256-column tiles (8-wave
+// workgroups sharing each K/V tile, with a four-stage copy ring; the fastest layout
+// measured on the 8K-prefix, 512-token step) unless they would be less than half full on
+// average, as in batches of mostly decode-like rows; then 128.
 int32_t auto_tile_cols(int32_t R, const int32_t* C, int32_t hq, int32_t hkv) {
   const int64_t g = hq / hkv;
+  bool decode = g <= s2l::kDecodeTileCols;
+  for (int32_t r = 0; r < R && decode; ++r) decode = (int64_t)C[r] * g <= s2l::kDecodeTileCols;
+  if (decode) return s2l::kDecodeTileCols;
   int64_t used = 0, alloc = 0;
   for (int32_t r = 0; r < R; ++r) {
     const int64_t cols = (int64_t)C[r] * g;
@@ -71,13 +75,15 @@ s2l_status resolve_opts(const s2l_plan_opts* o, bool need_cus, int32_t num_cus, 
   int32_t t = o ? o->target_items : 0, m = o ? o->min_split_keys : 0, x = o ? o->max_splits : 0;
   int32_t tc = o ? o->tile_cols : 0, kh = o ? o->key_halves : 0;
   if (t < 0 || m < 0 || x < 0) return fail(S2L_EINVAL, "plan opts must be >= 0");
-  if (tc != 0 && tc != s2l::kMinTileCols && tc != s2l::kMaxTileCols)
-    return fail(S2L_ENOTSUP, "tile_cols %d unsupported (0, 128 or 256)", tc);
+  if (tc != 0 && tc != s2l::kDecodeTileCols && tc != s2l::kMinTileCols && tc != s2l::kMaxTileCols)
+    return fail(S2L_ENOTSUP, "tile_cols %d unsupported (0, 16, 128 or 256)", tc);
+  if (tc == s2l::kDecodeTileCols && hq / hkv > s2l::kDecodeTileCols)
+    return fail(S2L_ENOTSUP, "16-column tiles need at most 16 query heads per kv head (have %d)", hq / hkv);
   if (kh < 0 || kh > 2) return fail(S2L_ENOTSUP, "key_halves %d unsupported (0, 1 or 2)", kh);
   r->tile_cols = tc != 0 ? tc : auto_tile_cols(R, C, hq, hkv);
-  if (r->tile_cols == s2l::kMaxTileCols && kh == 2)
+  if (r->tile_cols != s2l::kMinTileCols && kh == 2)
     return fail(S2L_ENOTSUP, "key_halves 2 needs 128-column tiles");
-  r->key_halves = kh != 0 ? kh : (r->tile_cols == s2l::kMaxTileCols ? 1 : 2);
+  r->key_halves = kh != 0 ? kh : (r->tile_cols == s2l::kMinTileCols ? 2 : 1);
   if (t == 0) {
     if (num_cus <= 0 && need_cus) {
       int dev = 0, n = 0;
@@ -270,8 +276,11 @@ s2l_status check_plan(const s2l_plan_info* plan, const s2l_batch* b, int32_t hq,
   if (plan->num_q_heads != hq || plan->num_kv_heads != hkv || plan->num_reqs != b->num_reqs ||
       plan->total_tokens != T)
     return fail(S2L_EINVAL, "plan was made for another batch or head count");
-  if (plan->tile_cols != s2l::kMinTileCols && plan->tile_cols != s2l::kMaxTileCols)
+  if (plan->tile_cols != s2l::kDecodeTileCols && plan->tile_cols != s2l::kMinTileCols &&
+      plan->tile_cols != s2l::kMaxTileCols)
     return fail(S2L_EINVAL, "plan info has an invalid tile width %d", plan->tile_cols);
+  if (plan->tile_cols == s2l::kDecodeTileCols && hq / hkv > s2l::kDecodeTileCols)
+    return fail(S2L_EINVAL, "plan info has 16-column tiles for %d query heads per kv head", hq / hkv);
   if (plan->key_halves != 1 && (plan->key_halves != 2 || plan->tile_cols != s2l::kMinTileCols))
     return fail(S2L_EINVAL, "plan info has an invalid key_halves %d", plan->key_halves);
   if (plan->num_items < 0 || plan->num_tiles < 0 || plan->part_floats < 0 ||
@@ -327,6 +336,26 @@ extern "C" {
 int32_t s2l_abi_version(void) { return S2L_ABI_VERSION; }
 
 const char* s2l_last_error(void) { return g_err.c_str(); }
+
+s2l_status s2l_calib_stream_read(const void* buf, size_t bytes, uint32_t* sink, int32_t grid, void* stream) {
+  if (!buf || !sink) return fail(S2L_EINVAL, "buffer or sink is NULL");
+  if (bytes == 0 || bytes % 16 != 0) return fail(S2L_EINVAL, "bytes must be a positive multiple of 16");
+  if (grid <= 0) return fail(S2L_EINVAL, "grid must be > 0");
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_stream_read(buf, bytes, sink, grid, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("stream_read launch", e);
+  return ok();
+}
+
+s2l_status s2l_calib_mfma_bf16(int64_t iters, float* sink, int32_t grid, int64_t* flops_out, void* stream) {
+  if (!sink) return fail(S2L_EINVAL, "sink is NULL");
+  if (iters <= 0 || grid <= 0) return fail(S2L_EINVAL, "iters and grid must be > 0");
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_mfma_loop(iters, sink, grid, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("mfma loop launch", e);
+  if (flops_out) *flops_out = s2l::mfma_loop_flops(iters, grid);
+  return ok();
+}
 
 s2l_status s2l_kv_append(const s2l_kv_cache* cache, const s2l_batch* batch, const void* k_new, const void* v_new,
                          void* stream) {

@@ -812,6 +812,7 @@ void launch_main_dtype(const AttnLaunch& a, hipStream_t stream) {
 
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream) {
   if (a.dims.num_items <= 0) return hipSuccess;
+  if (a.tile_cols == kDecodeTileCols) return launch_attn_decode(a, stream);
   if (a.kv.fp8) launch_main_dtype<true>(a, stream);
   else launch_main_dtype<false>(a, stream);
   return hipGetLastError();

@@ -42,6 +42,17 @@ struct PlanLaunch {
   int64_t ws_bytes;
   void* workspace;
 };
+// Measurement support (calib.hip): a streaming read of `bytes` (a multiple of 16) over
+// `grid` workgroups of 256 threads (sink: grid * 256 words), and a register-only loop of
+// bf16 MFMAs (sink: grid * 256 floats; mfma_loop_flops gives its flop count).
+hipError_t launch_stream_read(const void* buf, uint64_t bytes, uint32_t* sink, int32_t grid, hipStream_t stream);
+hipError_t launch_mfma_loop(int64_t iters, float* sink, int32_t grid, hipStream_t stream);
+int64_t mfma_loop_flops(int64_t iters, int32_t grid);
+
+// Attention for a plan of kDecodeTileCols-column items (decode_attn.hip).
+struct AttnLaunch;
+hipError_t launch_attn_decode(const AttnLaunch& a, hipStream_t stream);
+
 hipError_t launch_attn_plan(const PlanLaunch& a, const PlanDims& dims, hipStream_t stream);
 
 struct AttnLaunch {

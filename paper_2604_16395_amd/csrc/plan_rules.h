@@ -23,6 +23,7 @@ constexpr int kHeadDim = 128;
 constexpr int kPageSize = 16;
 constexpr int kMinTileCols = 128;   // packed (token, head) columns per work item: 4 waves x 32
 constexpr int kMaxTileCols = 256;   //   or 8 waves x 32
+constexpr int kDecodeTileCols = 16; // decode-shaped items: 16 columns, four waves over the keys
 constexpr int kKvTile = 64;         // keys per LDS tile
 constexpr int kMaxSplitsCap = 64;
 constexpr int kDefaultMinSplitKeys = 512;
@@ -32,9 +33,10 @@ constexpr int32_t kPlanMagic = 0x53324c50;  // "S2LP"
 // Work items resident per CU: a 128-column item is a 4-wave workgroup with a two-stage
 // K/V ring (64 KiB of LDS), two per CU, or with two key-range groups an 8-wave workgroup
 // with two such rings (128 KiB), one per CU; a 256-column item is an 8-wave workgroup with
-// a four-stage ring (128 KiB), one per CU.
+// a four-stage ring (128 KiB), one per CU; a 16-column item is a 4-wave workgroup whose
+// waves hold two tiles of K and V in registers each (up to 512 registers), one per CU.
 S2L_HD inline int32_t items_per_cu(int32_t tile_cols, int32_t key_halves) {
-  return tile_cols == kMaxTileCols || key_halves == 2 ? 1 : 2;
+  return tile_cols == kMaxTileCols || tile_cols == kDecodeTileCols || key_halves == 2 ? 1 : 2;
 }
 
 struct PlanHeader {           // first 256 bytes of the workspace

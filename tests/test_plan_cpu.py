@@ -89,9 +89,18 @@ def test_split_policy_on_the_named_workloads():
 
 
 def test_automatic_tile_width():
-    # decode-like rows (C * G = 4 columns per kv head) fill 256-column tiles to 1.6%: 128
+    # every request fits a 16-column tile (C * G <= 16): the decode kernel's tiles
     info, _ = s2l_plan_host([4000] * 16, [1] * 16, 32, 8, num_cus=256)
+    assert info.tile_cols == 16 and info.key_halves == 1
+    info, _ = s2l_plan_host([4000, 10], [4, 2], 32, 8, num_cus=256)      # 16 and 8 columns
+    assert info.tile_cols == 16 and info.num_tiles == 2 * 8
+    info, _ = s2l_plan_host([4000], [2], 64, 8, num_cus=256)             # G = 8: 16 columns
+    assert info.tile_cols == 16
+    # one request past 16 columns: decode-like rows fill 256-column tiles to 2%: 128
+    info, _ = s2l_plan_host([4000] * 15 + [4000], [1] * 15 + [5], 32, 8, num_cus=256)
     assert info.tile_cols == 128 and info.key_halves == 2
+    info, _ = s2l_plan_host([4000], [1], 32, 1, num_cus=256)             # G = 32 > 16
+    assert info.tile_cols == 128
     info, _ = s2l_plan_host([100, 5000], [300, 700], 32, 8, num_cus=256)
     assert info.tile_cols == 256 and info.key_halves == 1
 
@@ -112,6 +121,15 @@ def test_option_validation():
         s2l_plan_host([100], [10], 32, 8, plan_opts(tile_cols=256, key_halves=2))
     with pytest.raises(Exception):
         s2l_plan_host([100], [10], 32, 8, plan_opts(key_halves=3))
+    with pytest.raises(Exception):
+        s2l_plan_host([100], [1], 32, 8, plan_opts(tile_cols=16, key_halves=2))
+    with pytest.raises(Exception):
+        s2l_plan_host([100], [1], 32, 1, plan_opts(tile_cols=16))         # G = 32
+    with pytest.raises(Exception):
+        s2l_plan_host([100], [1], 32, 8, plan_opts(tile_cols=64))
+    # a 16-column tile holds 16 / G tokens: longer chunks take several tiles
+    info, _ = s2l_plan_host([100], [10], 32, 8, plan_opts(tile_cols=16, target_items=1))
+    assert info.num_tiles == 8 * 3 and info.num_items == 8 * 3
 
 
 def test_workspace_grows_with_partials_only_for_split_requests():
