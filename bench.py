@@ -108,6 +108,8 @@ def main():
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the other named workloads (config 2-5 timings in other_configs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-ceilings", action="store_true",
+                    help="skip the measured HBM-read and MFMA ceilings (calibration kernels)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (for counter calibration) and exit")
     args = ap.parse_args()
@@ -282,7 +284,7 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "kernel_source_sha256_16": src_hash},
     }
-    if not args.eager:
+    if not args.eager and not args.no_ceilings:
         from paper_2604_16395_amd.benchcfg import measured_ceilings
         ceil = measured_ceilings()
         ceil["attn_frac_of_measured_mfma"] = round(achieved / ceil["mfma_bf16_tflops"], 4)

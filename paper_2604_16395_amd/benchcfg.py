@@ -207,15 +207,21 @@ def cfg4(stream, gen):
                                 "work_items": dplan.num_items, "tile_cols": dplan.tile_cols}
         del d
         torch.cuda.empty_cache()
-        # 64 decode rows over 32K prefixes each (a steady decode batch)
-        P64, C64 = np.full(64, 32768, np.int32), np.ones(64, np.int32)
-        pool64 = int(((P64 + C64 + 15) // 16).sum() + 16)
-        d = Layer(P64, C64, 32, 8, pool64, tables_for(P64, C64, pool64, rng), gen, copies=2)
-        _, dus, dplan = measure_step(d, stream, 2)
-        res["decode_64x32k"] = {"attn_us": round(dus, 2), "kv_gbs": round(d.kv_bytes() / dus / 1e3, 1),
-                                "pct_hbm_peak": round(100 * d.kv_bytes() / dus / 1e3 / PEAK_HBM_GBS, 1),
-                                "work_items": dplan.num_items, "tile_cols": dplan.tile_cols}
+        res["decode_64x32k"] = decode_64x32k(stream, gen)
     return res
+
+
+def decode_64x32k(stream, gen, seed=1006):
+    """64 decode rows (C = 1) over 32K-token prefixes each, 32q/8kv: a steady decode batch,
+    bound by reading its 4.3 GB of K and V (two rotating pool copies)."""
+    P64, C64 = np.full(64, 32768, np.int32), np.ones(64, np.int32)
+    pool64 = int(((P64 + C64 + 15) // 16).sum() + 16)
+    d = Layer(P64, C64, 32, 8, pool64, tables_for(P64, C64, pool64, np.random.default_rng(seed)), gen, copies=2)
+    _, dus, dplan = measure_step(d, stream, 2)
+    return {"attn_us": round(dus, 2), "kv_gbs": round(d.kv_bytes() / dus / 1e3, 1),
+            "pct_hbm_peak": round(100 * d.kv_bytes() / dus / 1e3 / PEAK_HBM_GBS, 1),
+            "kv_bytes_per_launch": d.kv_bytes(), "io_bytes_per_launch": d.io_bytes(),
+            "work_items": dplan.num_items, "tile_cols": dplan.tile_cols}
 
 
 def cfg5(stream, gen):
@@ -322,3 +328,13 @@ def all_configs(seed=2024):
     except Exception as e:
         res["scheduler"] = {"error": f"{type(e).__name__}: {e}"}
     return res
+
+
+if __name__ == "__main__":
+    # one named workload on its own (for profiling): python -m paper_2604_16395_amd.benchcfg decode_64x32k
+    import json
+    import sys
+    g = torch.Generator(device="cuda")
+    g.manual_seed(2024)
+    fn = {"decode_64x32k": decode_64x32k, "config2": cfg2, "config5": cfg5}[sys.argv[1]]
+    print(json.dumps(fn(torch.cuda.Stream(), g)), flush=True)
