@@ -169,6 +169,16 @@ s2l_status s2l_kv_gather(const s2l_kv_cache* cache, const s2l_batch* batch, int3
                          const int32_t* cu_out, void* k_out, void* v_out, void* stream);
 
 /*
+ * Validation of block-table contents on the device, a debugging aid: the other calls assume
+ * the used entries are valid page ids and do not check them.  Counts the used entries of
+ * every request (logical pages 0 .. ceil((P + C) / 16) - 1) that lie outside
+ * [0, cache->num_pages).
+ *   counts: DEVICE int32 [2]; receives (number of such entries, 1 + the largest request
+ *           index that has one, or 0).  Asynchronous on `stream`; read after a sync.
+ */
+s2l_status s2l_check_tables(const s2l_kv_cache* cache, const s2l_batch* batch, int32_t* counts, void* stream);
+
+/*
  * Swap-out and swap-in of KV pages (Sec. 4.3: a preempted request's blocks move to CPU
  * memory and come back when it resumes; Sec. 4.2: blocks past an update's LCP are simply
  * dropped).  One layer's pages move between the device pools of `cache` and two pinned

@@ -23,7 +23,7 @@ from ._lib import (S2L_KV_BF16, S2L_KV_FP8_E4M3, S2LError, S2LLibraryMissing, s2
                    s2l_plan_opts)
 
 __all__ = ["PagedKVCache", "Batch", "plan_opts", "S2LError", "S2LLibraryMissing",
-           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in",
+           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in", "s2l_check_tables",
            "s2l_calib_stream_read", "s2l_calib_mfma_bf16", "s2l_attn_workspace_bytes",
            "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_attn_main", "s2l_split_reduce",
            "s2l_plan_host", "library_path"]
@@ -164,6 +164,13 @@ def s2l_kv_swap_out(cache, pairs, host_k, host_v, stream=None):
 def s2l_kv_swap_in(cache, pairs, host_k, host_v, stream=None):
     """Pinned host pages pairs[i][0] -> device pages pairs[i][1] (K and V)."""
     _swap("s2l_kv_swap_in", cache, pairs, host_k, host_v, stream)
+
+
+def s2l_check_tables(cache, batch, counts, stream=None):
+    """Count used block-table entries outside the pool into the device int32[2] `counts`."""
+    _check(counts, torch.int32, "counts")
+    cc, bc = cache.c(), batch.c()
+    _lib.call("s2l_check_tables", ctypes.byref(cc), ctypes.byref(bc), _ptr(counts), _stream(stream))
 
 
 def s2l_calib_stream_read(buf, sink, grid, stream=None):

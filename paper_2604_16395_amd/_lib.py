@@ -86,6 +86,7 @@ SIGNATURES = {
     "s2l_last_error": (ctypes.c_char_p, []),
     "s2l_kv_append": (c_i32, [P_cache, P_batch, c_vp, c_vp, c_vp]),
     "s2l_kv_gather": (c_i32, [P_cache, P_batch, c_i32, c_vp, c_vp, c_vp, c_vp]),
+    "s2l_check_tables": (c_i32, [P_cache, P_batch, c_vp, c_vp]),
     "s2l_kv_swap_out": (c_i32, [P_cache, c_vp, c_i32, c_vp, c_vp, c_i32, c_vp]),
     "s2l_kv_swap_in": (c_i32, [P_cache, c_vp, c_i32, c_vp, c_vp, c_i32, c_vp]),
     "s2l_attn_workspace_bytes": (c_i32, [P_batch, c_i32, c_i32, P_opts, ctypes.POINTER(ctypes.c_size_t)]),

@@ -164,6 +164,7 @@ s2l::KvLaunch kv_launch(const s2l_kv_cache* c, const s2l_batch* b) {
   a.max_pages = b->max_pages_per_req;
   a.hkv = c->num_kv_heads;
   a.num_reqs = b->num_reqs;
+  a.num_pages = c->num_pages;
   a.fp8 = c->dtype == S2L_KV_FP8_E4M3;
   return a;
 }
@@ -377,6 +378,23 @@ s2l_status s2l_kv_append(const s2l_kv_cache* cache, const s2l_batch* batch, cons
   hipError_t e = s2l::launch_kv_append(kv_launch(cache, batch), k_new, v_new, max_touched,
                                        static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("kv_append launch", e);
+  return ok();
+}
+
+s2l_status s2l_check_tables(const s2l_kv_cache* cache, const s2l_batch* batch, int32_t* counts, void* stream) {
+  s2l_status st;
+  int64_t T = 0;
+  if ((st = check_cache(cache, batch)) != S2L_OK) return st;
+  if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
+  if (!counts) return fail(S2L_EINVAL, "counts is NULL");
+  int32_t max_used = 0;
+  for (int32_t r = 0; r < batch->num_reqs; ++r) {
+    const int64_t n = (int64_t)batch->prefix_lens_host[r] + batch->chunk_lens_host[r];
+    max_used = std::max<int32_t>(max_used, (int32_t)((n + s2l::kPageSize - 1) / s2l::kPageSize));
+  }
+  (void)hipGetLastError();
+  hipError_t e = s2l::launch_check_tables(kv_launch(cache, batch), max_used, counts, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail("check_tables launch", e);
   return ok();
 }
 

@@ -108,7 +108,39 @@ __global__ __launch_bounds__(256) void kv_page_copy_kernel(
   }
 }
 
+// Table check: workgroup (page block, request) looks at 256 logical pages of the request's
+// used range [0, ceil((P + C) / 16)) and counts entries outside [0, num_pages) (vector
+// atomics into counts[0]; counts[1] keeps the largest request index with a bad entry + 1).
+__global__ __launch_bounds__(256) void check_tables_kernel(const int32_t* __restrict__ prefix_lens,
+                                                           const int32_t* __restrict__ chunk_lens,
+                                                           const int32_t* __restrict__ block_tables,
+                                                           int32_t max_pages, int32_t num_pages, int32_t* counts) {
+  const int r = blockIdx.y;
+  const int used = (prefix_lens[r] + chunk_lens[r] + 15) >> 4;
+  const int lp = blockIdx.x * 256 + threadIdx.x;
+  if (lp >= used || lp >= max_pages) return;
+  const int32_t page = block_tables[(int64_t)r * max_pages + lp];
+  if (page < 0 || page >= num_pages) {
+    atomicAdd(counts, 1);
+    atomicMax(counts + 1, r + 1);
+  }
+}
+
+__global__ void zero2_kernel(int32_t* counts) {
+  if (threadIdx.x < 2) counts[threadIdx.x] = 0;
+}
+
 }  // namespace
+
+hipError_t launch_check_tables(const KvLaunch& a, int32_t max_pages_used, int32_t* counts, hipStream_t stream) {
+  zero2_kernel<<<1, 64, 0, stream>>>(counts);
+  if (a.num_reqs > 0 && max_pages_used > 0) {
+    dim3 grid((max_pages_used + 255) / 256, a.num_reqs);
+    check_tables_kernel<<<grid, 256, 0, stream>>>(a.prefix_lens, a.chunk_lens, a.block_tables, a.max_pages,
+                                                  a.num_pages, counts);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_kv_page_copy(const void* src_k, const void* src_v, void* dst_k, void* dst_v,
                                const int32_t* pairs, int32_t n, int32_t num_src, int32_t num_dst,

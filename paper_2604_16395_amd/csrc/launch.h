@@ -19,6 +19,7 @@ struct KvLaunch {           // device pointers of one layer's cache and one batc
   int32_t max_pages;
   int32_t hkv;
   int32_t num_reqs;
+  int32_t num_pages;
   bool fp8;
 };
 
@@ -26,6 +27,9 @@ hipError_t launch_kv_append(const KvLaunch& a, const void* knew, const void* vne
                             hipStream_t stream);
 hipError_t launch_kv_gather(const KvLaunch& a, int32_t include_chunk, const int32_t* cu_out, void* kout,
                             void* vout, int32_t max_pages_read, hipStream_t stream);
+// Counts used block-table entries outside [0, num_pages) into counts[0] and the largest
+// offending request + 1 into counts[1] (both cleared first).
+hipError_t launch_check_tables(const KvLaunch& a, int32_t max_pages_used, int32_t* counts, hipStream_t stream);
 // Copies whole (page, all kv heads) runs of K and V from pages pairs[i][0] of the source
 // pools to pages pairs[i][1] of the destination pools (either side may be pinned host
 // memory); pairs is a device array; pairs outside [0, num_src) x [0, num_dst) are skipped.

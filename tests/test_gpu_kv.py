@@ -120,3 +120,29 @@ def test_swap_out_and_back_in_is_bit_exact():
     torch.cuda.synchronize()
     assert torch.equal(ko2.view(torch.int16), ko.view(torch.int16))
     assert torch.equal(vo2.view(torch.int16), vo.view(torch.int16))
+
+
+def test_check_tables_counts_bad_entries():
+    import paper_2604_16395_amd as s2l
+    num_pages = 20
+    kp = torch.zeros((num_pages, 2, 16, 128), dtype=torch.bfloat16, device="cuda")
+    cache = s2l.PagedKVCache(kp, kp.clone())
+    P = np.array([40, 0, 100, 5], np.int32)        # used pages: 3, 1, 7, 1
+    C = np.array([8, 16, 0, 0], np.int32)
+    tables = np.zeros((4, 8), np.int32)
+    tables[0, :3] = [1, 2, 3]
+    tables[0, 3:] = -7                               # past the used range: not checked
+    tables[1, 0] = num_pages                         # bad
+    tables[2, :7] = [4, -1, 5, 6, 7, 8, 1 << 30]     # two bad
+    tables[3, 0] = 19
+    batch = s2l.Batch(P, C, tables)
+    counts = torch.full((2,), 99, dtype=torch.int32, device="cuda")
+    s2l.s2l_check_tables(cache, batch, counts)
+    torch.cuda.synchronize()
+    assert counts.tolist() == [3, 3]
+    tables[1, 0] = 0
+    tables[2, 1] = 0
+    tables[2, 6] = 0
+    s2l.s2l_check_tables(cache, s2l.Batch(P, C, tables), counts)
+    torch.cuda.synchronize()
+    assert counts.tolist() == [0, 0]
