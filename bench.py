@@ -210,6 +210,17 @@ def main():
         "split_reduce": capture(lambda: [s2l.s2l_split_reduce(batch, HQ, out, lse, plan, ws, main_stream)
                                          for _ in range(L)]),
     }
+
+    # The same step with the append fused into the attention launch (s2l_append_chunk_prefill_attn:
+    # plan, then one call); reported beside the separate-call step, which stays the timed one so
+    # that the attention kernel's roofline and its trace are those of one launch kind.
+    def enqueue_fused_step(l):
+        plan_box["plan_f"] = s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, main_stream)
+        plan_box["fused"] = s2l.s2l_append_chunk_prefill_attn(caches[l], batch, k_new, v_new, q, HQ, scale, out,
+                                                               lse, plan_box["plan_f"], ws, main_stream)
+
+    fused_graph = None if args.eager else capture(
+        lambda: [enqueue_fused_step((args.warmup + i) % L) for i in range(args.steps)])
     torch.cuda.synchronize()
 
     if warm_graph is not None:
@@ -227,6 +238,16 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    fused_ms = None
+    if fused_graph is not None:
+        with torch.cuda.stream(main_stream):
+            fused_graph.replay()
+            f0, f1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            f0.record(main_stream)
+            fused_graph.replay()
+            f1.record(main_stream)
+        torch.cuda.synchronize()
+        fused_ms = f0.elapsed_time(f1) / args.steps
 
     # timed region 2: each kernel alone, L launches back to back per replay (average launch
     # duration, HIP events on the stream the kernels run on)
@@ -284,6 +305,11 @@ def main():
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic, "kernel_source_sha256_16": src_hash},
     }
+    if fused_ms is not None:
+        result["fused_append_step"] = {
+            "us_per_step": round(fused_ms * 1e3, 2), "tflops": round(flops / fused_ms / 1e9, 2),
+            "single_launch": bool(plan_box.get("fused")),
+            "what": "plan, then s2l_append_chunk_prefill_attn (append inside the attention launch, split merge)"}
     # The paper's own figures are end-to-end serving results (its traces, Llama-3.1-8B on
     # H200 with TP=2): context for the reader, not a target this kernel can be compared with.
     result["paper_context"] = {

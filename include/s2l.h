@@ -246,6 +246,23 @@ s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* ba
                                   void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * Append and attention of one step in one call (Sec. 4.2 / Sec. 5.1: the chunk's K/V join
+ * the cache and its queries attend to prefix and chunk): the same results as
+ * s2l_kv_append followed by s2l_chunk_prefill_attn (arguments as there; k_new / v_new
+ * bf16 [T][Hkv][128]), pages and outputs bit for bit.  When the cache is bf16, the plan's
+ * tiles are 128 or 256 columns and every P_r is a multiple of 16, it is one attention
+ * launch (plus the split merge): attention copies the chunk's own keys straight from
+ * k_new / v_new, and the first key-range piece of each (kv head, query tile) writes that
+ * tile's rows into the pages, which nothing in the launch reads; the append launch and its
+ * gap leave the step.  Otherwise it issues the two calls.  *fused_out (may be NULL) = 1
+ * if the single launch was used.
+ */
+s2l_status s2l_append_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* batch, const void* k_new,
+                                         const void* v_new, const void* q, int32_t num_q_heads, float softmax_scale,
+                                         void* out, float* lse, const s2l_plan_info* plan, void* workspace,
+                                         size_t ws_bytes, int32_t* fused_out, void* stream);
+
+/*
  * The main attention kernel alone (online softmax over the work items of the plan).
  * Unsplit requests get their final out/lse; split requests get fp32 partials (unnormalised
  * output, then reference max and running sum) in the workspace, merged by s2l_split_reduce.

@@ -23,8 +23,8 @@ from ._lib import (S2L_KV_BF16, S2L_KV_FP8_E4M3, S2LError, S2LLibraryMissing, s2
                    s2l_plan_opts)
 
 __all__ = ["PagedKVCache", "Batch", "plan_opts", "S2LError", "S2LLibraryMissing",
-           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in", "s2l_check_tables",
-           "s2l_calib_stream_read", "s2l_calib_mfma_bf16", "s2l_attn_workspace_bytes",
+           "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in",
+           "s2l_check_tables", "s2l_append_chunk_prefill_attn", "s2l_calib_stream_read", "s2l_calib_mfma_bf16", "s2l_attn_workspace_bytes",
            "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_attn_main", "s2l_split_reduce",
            "s2l_plan_host", "library_path"]
 
@@ -224,6 +224,22 @@ def s2l_chunk_prefill_attn(cache, batch, q, num_q_heads, softmax_scale, out, lse
                            stream=None):
     _attn("s2l_chunk_prefill_attn", cache, batch, q, num_q_heads, softmax_scale, out, lse, plan,
           workspace, stream)
+
+
+def s2l_append_chunk_prefill_attn(cache, batch, k_new, v_new, q, num_q_heads, softmax_scale, out, lse, plan,
+                                  workspace, stream=None):
+    """s2l_kv_append + s2l_chunk_prefill_attn, in one attention launch where possible;
+    returns True when the single launch was used."""
+    for t, n in ((k_new, "k_new"), (v_new, "v_new"), (q, "q"), (out, "out")):
+        _check(t, torch.bfloat16, n)
+    _check(lse, torch.float32, "lse")
+    _check(workspace, torch.uint8, "workspace")
+    cc, bc = cache.c(), batch.c()
+    fused = ctypes.c_int32()
+    _lib.call("s2l_append_chunk_prefill_attn", ctypes.byref(cc), ctypes.byref(bc), _ptr(k_new), _ptr(v_new),
+              _ptr(q), num_q_heads, float(softmax_scale), _ptr(out), _ptr(lse), ctypes.byref(plan),
+              _ptr(workspace), workspace.numel(), ctypes.byref(fused), _stream(stream))
+    return bool(fused.value)
 
 
 def s2l_attn_main(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, stream=None):

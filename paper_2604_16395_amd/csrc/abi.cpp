@@ -308,7 +308,7 @@ s2l_status attn_common(const s2l_kv_cache* cache, const s2l_batch* batch, const 
 
 s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q, int32_t num_q_heads,
                        float softmax_scale, void* out, float* lse, const s2l_plan_info* plan, void* workspace,
-                       size_t ws_bytes, void* stream) {
+                       size_t ws_bytes, void* stream, const void* k_new = nullptr, const void* v_new = nullptr) {
   int64_t T = 0;
   s2l_status st = attn_common(cache, batch, q, num_q_heads, softmax_scale, out, plan, workspace, ws_bytes, &T);
   if (st != S2L_OK) return st;
@@ -324,6 +324,8 @@ s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const 
   a.tile_cols = plan->tile_cols;
   a.key_halves = plan->key_halves;
   a.group_by_xcd = (plan->flags & S2L_PLAN_UNIFORM) != 0;
+  a.knew = k_new;
+  a.vnew = v_new;
   (void)hipGetLastError();
   hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("attn_main launch", e);
@@ -551,6 +553,29 @@ s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* o
   hipError_t e = s2l::launch_split_reduce(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("split_reduce launch", e);
   return ok();
+}
+
+s2l_status s2l_append_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* batch, const void* k_new,
+                                         const void* v_new, const void* q, int32_t num_q_heads, float softmax_scale,
+                                         void* out, float* lse, const s2l_plan_info* plan, void* workspace,
+                                         size_t ws_bytes, int32_t* fused_out, void* stream) {
+  s2l_status st;
+  int64_t T = 0;
+  if ((st = check_cache(cache, batch)) != S2L_OK) return st;
+  if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
+  if (T > 0 && (!k_new || !v_new)) return fail(S2L_EINVAL, "k_new/v_new is NULL");
+  bool fuse = cache->dtype == S2L_KV_BF16 && plan && plan->tile_cols != s2l::kDecodeTileCols;
+  for (int32_t r = 0; r < batch->num_reqs && fuse; ++r) fuse = batch->prefix_lens_host[r] % s2l::kPageSize == 0;
+  if (fused_out) *fused_out = fuse ? 1 : 0;
+  if (!fuse) {
+    if ((st = s2l_kv_append(cache, batch, k_new, v_new, stream)) != S2L_OK) return st;
+    return s2l_chunk_prefill_attn(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes,
+                                  stream);
+  }
+  st = attn_launch(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes, stream,
+                   T > 0 ? k_new : nullptr, T > 0 ? v_new : nullptr);
+  if (st != S2L_OK) return st;
+  return s2l_split_reduce(batch, num_q_heads, out, lse, plan, workspace, ws_bytes, stream);
 }
 
 s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q,

@@ -155,9 +155,10 @@ struct Ring {
 template <bool kFp8, int kColWaves, int kHalves>
 __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)) void attn_main_kernel(
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out, float* __restrict__ lse,
-    const void* __restrict__ kpool, const void* __restrict__ vpool, const float* __restrict__ kscale,
+    void* kpool, void* vpool, const float* __restrict__ kscale,
     const float* __restrict__ vscale, const int32_t* __restrict__ block_tables, int32_t max_pages, int32_t hq,
-    int32_t hkv, float scale_log2, PlanPtrs pv, int32_t group_by_xcd) {
+    int32_t hkv, float scale_log2, PlanPtrs pv, int32_t group_by_xcd, const uint16_t* __restrict__ knew,
+    const uint16_t* __restrict__ vnew) {
   using RingT = Ring<kFp8, kColWaves, kHalves>;
   constexpr int kWaves = kColWaves * kHalves;
   constexpr int kS = RingT::kStages;
@@ -250,6 +251,12 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   const int pw = cw / kQuarters;
   const int s0 = (cw % kQuarters) * kRowsPerWave;
   uint32_t kvo[kFp8 ? kF8Loads : kDma], vvo[kFp8 ? kF8Loads : kDma];
+  // Fused append (bf16, page-aligned prefixes): keys at or past P, the chunk's own, are
+  // copied straight from the new K/V rows (row stride hkv * 256 bytes) instead of the pages,
+  // which this same launch writes; kno / vno are the lane offsets for that source.
+  const bool fused = !kFp8 && knew != nullptr;
+  const uint32_t new_stride = (uint32_t)hkv * kRowBytes;
+  uint32_t kno[kFp8 ? 1 : kDma], vno[kFp8 ? 1 : kDma];
   if constexpr (!kFp8) {
     // LDS-direct load d writes tile rows 16 pw + s0 + 4d + (l >> 4), chunk l & 15: it
     // fetches the source chunk that the row's permutation puts there.
@@ -258,6 +265,8 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       const int slot = s0 + 4 * d + (lane >> 4), c = lane & 15;
       kvo[d] = slot * kRowBytes + ((c ^ slot) << 4);
       vvo[d] = slot * kRowBytes + ((c ^ ((slot & 3) << 2)) << 4);
+      kno[d] = slot * new_stride + ((c ^ slot) << 4);
+      vno[d] = slot * new_stride + ((c ^ ((slot & 3) << 2)) << 4);
     }
   } else {
     // lane l loads bytes [16 f, 16 f + 16) of key slot s0 + l / kLpr (f as below)
@@ -296,10 +305,27 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   auto page_of = [&](int j) -> int32_t { return readlane_ordered(pg_win, j - win0); };
 
   // Page pg of the tile at key kb into the buffer at LDS byte `dst` (bf16: LDS-direct).
-  auto dma_rows = [&](const char* base, int32_t pg, int kb, int dst, const uint32_t* vo) {
-    const int bytes = __builtin_amdgcn_readfirstlane(clamp16(hi - (kb + 16 * pw)) * kKeyBytes);
-    const i32x4 rs = sgpr_rsrc(base + (int64_t)pg * page_stride, bytes);
+  auto dma_rows = [&](bool is_k, int32_t pg, int kb, int dst) {
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)smem;
+    const int key0 = kb + 16 * pw;
+    const int n = clamp16(hi - key0);
+    if (fused && key0 >= P) {
+      // chunk rows of this kv head: new row (row0 + key0 - P + slot), one per key
+      const char* nb = reinterpret_cast<const char*>(is_k ? knew : vnew) +
+                       ((int64_t)(row0 + key0 - P) * hkv + g) * kRowBytes;
+      const int bytes = __builtin_amdgcn_readfirstlane(n > 0 ? (n - 1) * (int)new_stride + kRowBytes : 0);
+      const i32x4 rs = sgpr_rsrc(nb, bytes);
+      const uint32_t* no = is_k ? kno : vno;
+#pragma unroll
+      for (int d = 0; d < kDma; ++d) {
+        const int row = 16 * pw + s0 + 4 * d;
+        lds_dma_b128(rs, no[d], __builtin_amdgcn_readfirstlane(lds0 + grp_base + dst + row * kRowBytes));
+      }
+      return;
+    }
+    const int bytes = __builtin_amdgcn_readfirstlane(n * kKeyBytes);
+    const i32x4 rs = sgpr_rsrc((is_k ? kpb : vpb) + (int64_t)pg * page_stride, bytes);
+    const uint32_t* vo = is_k ? kvo : vvo;
 #pragma unroll
     for (int d = 0; d < kDma; ++d) {
       const int row = 16 * pw + s0 + 4 * d;
@@ -513,8 +539,8 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       // finished iteration t - 1, whose stages the copies below overwrite.
       wait_vmcnt<(2 * kS - 4) * kDma>();
       __builtin_amdgcn_s_barrier();
-      dma_rows(vpb, pg_klast, lo + (t + kS - 1) * kKvTile, kVBase + ((kJ + kS - 1) % kS) * kTileBytes, vvo);
-      dma_rows(kpb, pg_knext, lo + (t + kS) * kKvTile, kKBase + kJ * kTileBytes, kvo);
+      dma_rows(false, pg_klast, lo + (t + kS - 1) * kKvTile, kVBase + ((kJ + kS - 1) % kS) * kTileBytes);
+      dma_rows(true, pg_knext, lo + (t + kS) * kKvTile, kKBase + kJ * kTileBytes);
       pg_klast = pg_knext;
       advance_window(t + kS + 1);
       pg_knext = page_of(t + kS + 1);
@@ -563,6 +589,24 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     }
   };
 
+  // Fused append: the first key-range piece of each (kv head, query tile) writes the tile's
+  // chunk rows of kv head g into their pages (slots P + i, i in [i0, i1)); nothing in this
+  // launch reads those slots from the pages.  Its loads and stores overlap the Q loads and
+  // are covered by the wait below.
+  if (fused && it.s == 0) {
+    constexpr int kThreads = kWaves * 64;
+    const int units = (i1 - i0) * 2 * 16;   // (token, K or V, 16-byte chunk)
+    for (int u = threadIdx.x; u < units; u += kThreads) {
+      const int c = u & 15, kv = (u >> 4) & 1, i = i0 + (u >> 5);
+      const int pos = P + i;
+      const int64_t page = bt[pos >> 4];
+      const uint16_t* src = (kv ? vnew : knew) + ((int64_t)(row0 + i) * hkv + g) * kHeadDim + 8 * c;
+      char* dst = static_cast<char*>(kv ? vpool : kpool) +
+                  ((page * hkv + g) * 16 + (pos & 15)) * kRowBytes + 16 * c;
+      *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+    }
+  }
+
   // Page ids of the first tiles are requested while the Q loads are in flight; the Q loads
   // are then waited for on every path, before any LDS-direct copy is issued: the compiler's
   // wait-count bookkeeping does not see those copies, and a Q load it still counted as
@@ -580,10 +624,10 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     if constexpr (!kFp8) {
 #pragma unroll
       for (int j = 0; j < kS - 1; ++j) {
-        dma_rows(kpb, pg[j], lo + j * kKvTile, kKBase + j * kTileBytes, kvo);
-        dma_rows(vpb, pg[j], lo + j * kKvTile, kVBase + j * kTileBytes, vvo);
+        dma_rows(true, pg[j], lo + j * kKvTile, kKBase + j * kTileBytes);
+        dma_rows(false, pg[j], lo + j * kKvTile, kVBase + j * kTileBytes);
       }
-      dma_rows(kpb, pg[kS - 1], lo + (kS - 1) * kKvTile, kKBase + (kS - 1) * kTileBytes, kvo);
+      dma_rows(true, pg[kS - 1], lo + (kS - 1) * kKvTile, kKBase + (kS - 1) * kTileBytes);
       pg_klast = pg[kS - 1];
       pg_knext = pg[kS];
       wait_vmcnt<(2 * kS - 2) * kDma>();   // K(0), the first of these copies
@@ -800,7 +844,8 @@ void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
   attn_main_kernel<kFp8, kColWaves, kHalves><<<(unsigned)a.dims.num_items, kColWaves * kHalves * 64, 0, stream>>>(
       static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
       a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, a.softmax_scale * kLog2e,
-      plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0);
+      plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0, static_cast<const uint16_t*>(a.knew),
+      static_cast<const uint16_t*>(a.vnew));
 }
 
 template <bool kFp8>

@@ -71,6 +71,8 @@ struct AttnLaunch {
   int32_t tile_cols;        // 128 or 256 (host copy of the plan's tile width)
   int32_t key_halves;       // 1 or 2 wave groups per item, each on half of its key range
   bool group_by_xcd;        // items of near-equal cost: consecutive items onto one XCD
+  const void* knew = nullptr;   // fused append (bf16, page-aligned prefixes): the chunk's
+  const void* vnew = nullptr;   //   new K/V rows [T][Hkv][128], else null
 };
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream);
 
