@@ -6,6 +6,7 @@ an fp8 cache: E4M3 codes with per-kv-head scales max|X_h| / 448).  Every timed r
 HIP graph of the launches, replayed, with HIP events on its stream around the replays.
 """
 import math
+import time
 
 import numpy as np
 import torch
@@ -81,13 +82,21 @@ class Layer:
         return self.kv_bytes() + float(self.C.sum()) * self.hq * 128 * 2 * 2
 
 
-def timed_graph(fn, stream, reps=5):
-    """Average ms of one replay of a graph of fn's launches (after one warm-up replay)."""
+def timed_graph(fn, stream, reps=5, settle=0.25):
+    """Average ms of one replay of a graph of fn's launches, after untimed replays for `settle`
+    seconds (at least one) so that the clock has reached its loaded steady state."""
     g = torch.cuda.CUDAGraph()
     with torch.cuda.stream(stream):
         with torch.cuda.graph(g, stream=stream):
             fn()
-        g.replay()
+    t0 = time.perf_counter()
+    while True:
+        with torch.cuda.stream(stream):
+            g.replay()
+        stream.synchronize()
+        if time.perf_counter() - t0 >= settle:
+            break
+    with torch.cuda.stream(stream):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
         for _ in range(reps):
