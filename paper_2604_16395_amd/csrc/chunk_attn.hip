@@ -152,7 +152,7 @@ struct Ring {
   static constexpr int kBytes = kHalves * kGroupBytes;
 };
 
-template <bool kFp8, int kColWaves, int kHalves>
+template <bool kFp8, int kColWaves, int kHalves, bool kFused>
 __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)) void attn_main_kernel(
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out, float* __restrict__ lse,
     void* kpool, void* vpool, const float* __restrict__ kscale,
@@ -243,8 +243,14 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     const int j = lane & 15, b4 = (lane >> 4) & 1;
     const int row = 4 * half + (j >> 2);
 #pragma unroll
-    for (int db = 0; db < 4; ++db)
-      va[db] = grp_base + row * kRowBytes + ((4 * (db ^ ((j >> 2) & 3)) + 2 * b4 + ((j >> 1) & 1)) << 4) + 8 * (j & 1);
+    for (int db = 0; db < 4; ++db) {
+      // The V stages start at kVBase (64 KiB with four stages): that base is added here, and
+      // hidden from constant folding, so that the offsets within the V ring (below 64 KiB)
+      // fit the LDS instructions' 16-bit immediate instead of costing an add per read.
+      va[db] = kVBase + grp_base + row * kRowBytes + ((4 * (db ^ ((j >> 2) & 3)) + 2 * b4 + ((j >> 1) & 1)) << 4) +
+               8 * (j & 1);
+      __asm__ volatile("" : "+v"(va[db]));
+    }
   }
 
   // Tile loads: column wave cw moves rows [s0, s0 + kRowsPerWave) of page pw of each tile.
@@ -254,7 +260,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   // Fused append (bf16, page-aligned prefixes): keys at or past P, the chunk's own, are
   // copied straight from the new K/V rows (row stride hkv * 256 bytes) instead of the pages,
   // which this same launch writes; kno / vno are the lane offsets for that source.
-  const bool fused = !kFp8 && knew != nullptr;
+  static_assert(!(kFp8 && kFused), "the fused append is for bf16 pages");
   const uint32_t new_stride = (uint32_t)hkv * kRowBytes;
   uint32_t kno[kFp8 ? 1 : kDma], vno[kFp8 ? 1 : kDma];
   if constexpr (!kFp8) {
@@ -309,7 +315,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void*)smem;
     const int key0 = kb + 16 * pw;
     const int n = clamp16(hi - key0);
-    if (fused && key0 >= P) {
+    if (kFused && key0 >= P) {
       // chunk rows of this kv head: new row (row0 + key0 - P + slot), one per key
       const char* nb = reinterpret_cast<const char*>(is_k ? knew : vnew) +
                        ((int64_t)(row0 + key0 - P) * hkv + g) * kRowBytes;
@@ -377,7 +383,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   };
   // One A fragment of O^T += V^T P^T: keys 16 k2 + (4-key sets of this lane half), d-block db.
   auto read_v = [&](int vofs, int k2, int db) {
-    const uint8_t* base = smem + vofs + 16 * k2 * kRowBytes + va[db];
+    const uint8_t* base = smem + (vofs - kVBase) + 16 * k2 * kRowBytes + va[db];
     const v4i16 x = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base));
     const v4i16 y = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + 8 * kRowBytes));
     const u32x2 ux = __builtin_bit_cast(u32x2, x), uy = __builtin_bit_cast(u32x2, y);
@@ -413,7 +419,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   // in the same tile (with_next), slots 6 and 7 also read that step's first two operands
   // (at nkofs / nvofs) into nxt, so its reads are not exposed behind its softmax prologue.
   auto step_main = [&](const f32x16& s, const u32x4* pp, u32x4* po, int kofs, int vofs, const Pre& f,
-                       auto with_qk, float& lsum, auto with_next, int nkofs, int nvofs, Pre& nxt) {
+                       auto with_qk, float& lsum, auto with_next, int nkofs, int nvofs, Pre& nxt, auto&& hook) {
     constexpr bool kQK = decltype(with_qk)::value;
     constexpr bool kNext = decltype(with_next)::value;
     f32x16 sn = f32x16{};
@@ -441,6 +447,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       po[i >> 2][i & 3] = pk;
       if (i & 1) l1 = sum_bf16x2(pk, l1);
       else l0 = sum_bf16x2(pk, l0);
+      if (i == 1) hook();
     }
     lsum = l0 + l1;
     __asm__ volatile("" ::"v"(po[0]), "v"(po[1]), "v"(lsum));   // produced here, not sunk
@@ -539,11 +546,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       // finished iteration t - 1, whose stages the copies below overwrite.
       wait_vmcnt<(2 * kS - 4) * kDma>();
       __builtin_amdgcn_s_barrier();
-      dma_rows(false, pg_klast, lo + (t + kS - 1) * kKvTile, kVBase + ((kJ + kS - 1) % kS) * kTileBytes);
-      dma_rows(true, pg_knext, lo + (t + kS) * kKvTile, kKBase + kJ * kTileBytes);
-      pg_klast = pg_knext;
       advance_window(t + kS + 1);
-      pg_knext = page_of(t + kS + 1);
     } else {
       wait_lgkmcnt0();
       __builtin_amdgcn_s_barrier();   // the stores of iteration t - 1 are visible
@@ -554,6 +557,17 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       pg_knext = page_of(t + 3);
     }
 
+    // The copies into the stages just freed are issued from inside the first step (after its
+    // second slot), where the MFMAs already in flight hide their scalar address work.
+    auto copies = [&]() {
+      if constexpr (!kFp8) {
+        dma_rows(false, pg_klast, lo + (t + kS - 1) * kKvTile, kVBase + ((kJ + kS - 1) % kS) * kTileBytes);
+        dma_rows(true, pg_knext, lo + (t + kS) * kKvTile, kKBase + kJ * kTileBytes);
+        pg_klast = pg_knext;
+        pg_knext = page_of(t + kS + 1);
+      }
+    };
+    auto no_hook = []() {};
     const int sb1 = lo + (2 * t + 1) * 32;
     constexpr std::true_type kWithQK{}, kWithNext{};
     constexpr std::false_type kNoNext{};
@@ -565,7 +579,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       mask(sc, sb1);
       float ls;
       const f32x16 sn =
-          step_main(sc, pa, pb, kcur, vcur, f, kWithQK, ls, kWithNext, kcur + kSubBytes, vcur + kSubBytes, f2);
+          step_main(sc, pa, pb, kcur, vcur, f, kWithQK, ls, kWithNext, kcur + kSubBytes, vcur + kSubBytes, f2, copies);
       sp = sc;
       sc = sn;
       lsum_p = ls;
@@ -576,7 +590,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
       mask(sc, sb1 + 32);
       float ls;
       const f32x16 sn =
-          step_main(sc, pb, pa, kcur + kSubBytes, vcur + kSubBytes, f2, kWithQK, ls, kNoNext, 0, 0, f2);
+          step_main(sc, pb, pa, kcur + kSubBytes, vcur + kSubBytes, f2, kWithQK, ls, kNoNext, 0, 0, f2, no_hook);
       sp = sc;
       sc = sn;
       lsum_p = ls;
@@ -593,7 +607,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   // chunk rows of kv head g into their pages (slots P + i, i in [i0, i1)); nothing in this
   // launch reads those slots from the pages.  Its loads and stores overlap the Q loads and
   // are covered by the wait below.
-  if (fused && it.s == 0) {
+  if (kFused && it.s == 0) {
     constexpr int kThreads = kWaves * 64;
     const int units = (i1 - i0) * 2 * 16;   // (token, K or V, 16-byte chunk)
     for (int u = threadIdx.x; u < units; u += kThreads) {
@@ -696,7 +710,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     settle(sp, pa, lsum_p);
     mask(sc, lo + (2 * t + 1) * 32);
     float ls;
-    step_main(sc, pa, pb, 0, vlast, f, kNoQK, ls, std::false_type{}, 0, 0, f);
+    step_main(sc, pa, pb, 0, vlast, f, kNoQK, ls, std::false_type{}, 0, 0, f, [] {});
     settle(sc, pb, ls);
     pv_acc(pb, vlast + kSubBytes);
   }
@@ -839,9 +853,9 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(uint16_t* __restrict_
 
 }  // namespace
 
-template <bool kFp8, int kColWaves, int kHalves>
+template <bool kFp8, int kColWaves, int kHalves, bool kFused>
 void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
-  attn_main_kernel<kFp8, kColWaves, kHalves><<<(unsigned)a.dims.num_items, kColWaves * kHalves * 64, 0, stream>>>(
+  attn_main_kernel<kFp8, kColWaves, kHalves, kFused><<<(unsigned)a.dims.num_items, kColWaves * kHalves * 64, 0, stream>>>(
       static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
       a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, a.softmax_scale * kLog2e,
       plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0, static_cast<const uint16_t*>(a.knew),
@@ -850,9 +864,17 @@ void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
 
 template <bool kFp8>
 void launch_main_dtype(const AttnLaunch& a, hipStream_t stream) {
-  if (a.tile_cols == kMaxTileCols) launch_main_variant<kFp8, 8, 1>(a, stream);
-  else if (a.key_halves == 2) launch_main_variant<kFp8, 4, 2>(a, stream);
-  else launch_main_variant<kFp8, 4, 1>(a, stream);
+  constexpr bool kF = false;
+  if (!kFp8 && a.knew != nullptr) {
+    // append fused into this launch (bf16 pages only)
+    if (a.tile_cols == kMaxTileCols) launch_main_variant<false, 8, 1, true>(a, stream);
+    else if (a.key_halves == 2) launch_main_variant<false, 4, 2, true>(a, stream);
+    else launch_main_variant<false, 4, 1, true>(a, stream);
+    return;
+  }
+  if (a.tile_cols == kMaxTileCols) launch_main_variant<kFp8, 8, 1, kF>(a, stream);
+  else if (a.key_halves == 2) launch_main_variant<kFp8, 4, 2, kF>(a, stream);
+  else launch_main_variant<kFp8, 4, 1, kF>(a, stream);
 }
 
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream) {
