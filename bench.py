@@ -97,7 +97,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--prefix", type=int, default=8192)
     ap.add_argument("--chunk", type=int, default=512)
-    ap.add_argument("--layers", type=int, default=32, help="KV pool copies rotated over the steps")
+    ap.add_argument("--layers", type=int, default=32,
+                    help="model layers per step (one KV pool each): a step plans once, then runs every layer")
     ap.add_argument("--tile-cols", type=int, default=0, help="query columns per work item (0 = library default)")
     ap.add_argument("--key-halves", type=int, default=0,
                     help="wave groups per work item splitting its key range (0 = library default)")
@@ -169,16 +170,19 @@ def main():
     main_stream = torch.cuda.Stream()
     torch.cuda.synchronize()
 
-    # One step for layer copy l, in stream order: append, plan, attention, split merge.  (A
-    # plan on a forked stream beside the append measured slower inside a graph: the
-    # cross-stream dependencies cost more than the overlap saves.)
+    # One step = one scheduler step of an L-layer model over this batch, in stream order: the
+    # plan (it depends on the batch's lengths only, so one plan serves every layer), then for
+    # each layer l: append of the chunk's K/V into layer l's pages, attention over them, split
+    # merge.  (A plan on a forked stream beside the first append measured slower inside a
+    # graph: the cross-stream dependencies cost more than the overlap saves.)
     plan_box = {}
 
-    def enqueue_step(l):
-        s2l.s2l_kv_append(caches[l], batch, k_new, v_new, main_stream)
+    def enqueue_step(_=None):
         plan_box["plan"] = s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, main_stream)
-        s2l.s2l_attn_main(caches[l], batch, q, HQ, scale, out, lse, plan_box["plan"], ws, main_stream)
-        s2l.s2l_split_reduce(batch, HQ, out, lse, plan_box["plan"], ws, main_stream)
+        for l in range(L):
+            s2l.s2l_kv_append(caches[l], batch, k_new, v_new, main_stream)
+            s2l.s2l_attn_main(caches[l], batch, q, HQ, scale, out, lse, plan_box["plan"], ws, main_stream)
+            s2l.s2l_split_reduce(batch, HQ, out, lse, plan_box["plan"], ws, main_stream)
 
     # Every launch is captured once into HIP graphs and replayed, so that the timed regions
     # measure the GPU, not the host's launch rate.
@@ -203,8 +207,8 @@ def main():
     torch.cuda.synchronize()
     plan = plan_box["plan"]
     # the warm-up steps and the K timed steps, one graph each (steps rotate over the layer copies)
-    warm_graph = capture(lambda: [enqueue_step(i % L) for i in range(args.warmup)]) if args.warmup else None
-    timed_graph = capture(lambda: [enqueue_step((args.warmup + i) % L) for i in range(args.steps)])
+    warm_graph = capture(lambda: [enqueue_step() for _ in range(args.warmup)]) if args.warmup else None
+    timed_graph = capture(lambda: [enqueue_step() for _ in range(args.steps)])
     kernel_graphs = {
         "append": capture(lambda: [s2l.s2l_kv_append(caches[l], batch, k_new, v_new, main_stream) for l in range(L)]),
         "plan": capture(lambda: [s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, main_stream) for _ in range(L)]),
@@ -217,13 +221,14 @@ def main():
     # The same step with the append fused into the attention launch (s2l_append_chunk_prefill_attn:
     # plan, then one call); reported beside the separate-call step, which stays the timed one so
     # that the attention kernel's roofline and its trace are those of one launch kind.
-    def enqueue_fused_step(l):
+    def enqueue_fused_step():
         plan_box["plan_f"] = s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, main_stream)
-        plan_box["fused"] = s2l.s2l_append_chunk_prefill_attn(caches[l], batch, k_new, v_new, q, HQ, scale, out,
-                                                               lse, plan_box["plan_f"], ws, main_stream)
+        for l in range(L):
+            plan_box["fused"] = s2l.s2l_append_chunk_prefill_attn(caches[l], batch, k_new, v_new, q, HQ, scale,
+                                                                   out, lse, plan_box["plan_f"], ws, main_stream)
 
     fused_graph = None if args.eager else capture(
-        lambda: [enqueue_fused_step((args.warmup + i) % L) for i in range(args.steps)])
+        lambda: [enqueue_fused_step() for _ in range(args.steps)])
     torch.cuda.synchronize()
 
     # Settle: an idle GPU starts a burst at a lower clock and takes about a second of load to
@@ -284,8 +289,9 @@ def main():
     # the step's outputs come from the graphs: check that the last replay left finite values
     assert torch.isfinite(out.float()).all(), "non-finite attention output"
 
-    flops = workloads.attn_flops([P], [C], HQ)
-    value = flops / (ms_per_step * 1e-3) / 1e12
+    flops = workloads.attn_flops([P], [C], HQ)             # one layer
+    ms_per_layer = ms_per_step / L
+    value = flops / (ms_per_layer * 1e-3) / 1e12
     achieved = flops / (main_ms * 1e-3) / 1e12
     src_hash = kernel_source_hash()
     traffic = traffic_from_profile(src_hash)
@@ -304,11 +310,14 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded N(0, 0.5^2) bf16 Q/K/V, random page permutation)",
         "config": {"workload": f"one request, P={P} cached + C={C} new tokens, 32q/8kv heads, d=128, "
-                               f"bf16 KV, 16-token pages, {L} rotating layer copies",
-                   "prefix": P, "chunk": C, "num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": 128},
-        "us_per_chunk": round(ms_per_step * 1e3, 2),
+                               f"bf16 KV, 16-token pages, {L} layers per step (one plan, then append + "
+                               f"attention + split merge per layer)",
+                   "layers_per_step": L, "prefix": P, "chunk": C, "num_q_heads": HQ, "num_kv_heads": HKV, "head_dim": 128},
+        "us_per_chunk": round(ms_per_layer * 1e3, 2),
         "pct_mfma_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "step_breakdown_us": step_breakdown,
+        "step_structure": f"plan once per step, then {L} x (append, attention, split merge); step_breakdown_us "
+                          f"gives each kernel's average launch",
         "timing": ("direct launches (--eager)" if args.eager else
                    "one HIP graph of the K steps, replayed once; per-kernel times are averages over "
                    "graphs of back-to-back launches of that kernel"),
@@ -323,7 +332,8 @@ def main():
     }
     if fused_ms is not None:
         result["fused_append_step"] = {
-            "us_per_step": round(fused_ms * 1e3, 2), "tflops": round(flops / fused_ms / 1e9, 2),
+            "us_per_step": round(fused_ms * 1e3, 2), "us_per_layer": round(fused_ms * 1e3 / L, 2),
+            "tflops": round(flops * L / fused_ms / 1e9, 2),
             "single_launch": bool(plan_box.get("fused")),
             "what": "plan, then s2l_append_chunk_prefill_attn (append inside the attention launch, split merge)"}
     # The paper's own figures are end-to-end serving results (its traces, Llama-3.1-8B on
