@@ -85,9 +85,26 @@ def cpu_baseline(case, min_seconds=10.0, max_reps=5):
             break
     import workloads as wl
     flops = wl.attn_flops(case.prefix_lens, case.chunk_lens, case.num_q_heads) * reps
-    return {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"whole workload (512 rows x 32 heads, fp64 numpy, blocked two-pass), {reps} rep(s), "
-                      f"{el:.1f} s"}
+    res = {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"whole workload (512 rows x 32 heads, fp64 numpy, blocked two-pass), {reps} rep(s), "
+                     f"{el:.1f} s"}
+    # the same oracle on one core, over every 8th chunk row (its keys are the same prefix plus
+    # the causal part up to the row): FLOPs of exactly those rows
+    try:
+        from threadpoolctl import threadpool_limits
+        rows = {0: list(range(0, int(case.chunk_lens[0]), 8))}
+        P0 = int(case.prefix_lens[0])
+        f1 = 4.0 * 128 * case.num_q_heads * sum(P0 + i + 1 for i in rows[0])
+        with threadpool_limits(1):
+            t1 = time.perf_counter()
+            ref_batch_attn(q, kp, vp, case.block_tables, case.prefix_lens, case.chunk_lens, case.cu_chunk,
+                           case.num_q_heads, 1.0 / np.sqrt(128.0), sample_rows=rows)
+            e1 = time.perf_counter() - t1
+        res["one_core"] = {"value": f1 / e1 / 1e12, "unit": "TFLOP/s", "cores": 1,
+                           "sample": f"every 8th chunk row ({len(rows[0])} rows x 32 heads), {e1:.1f} s"}
+    except ImportError:
+        pass
+    return res
 
 
 def main():
@@ -216,6 +233,9 @@ def main():
                                                         main_stream) for l in range(L)]),
         "split_reduce": capture(lambda: [s2l.s2l_split_reduce(batch, HQ, out, lse, plan, ws, main_stream)
                                          for _ in range(L)]),
+        # warm: every launch reads layer 0's pool, which then stays in the 256 MB last-level cache
+        "attn_main_warm": capture(lambda: [s2l.s2l_attn_main(caches[0], batch, q, HQ, scale, out, lse, plan, ws,
+                                                             main_stream) for _ in range(L)]),
     }
 
     # The same step with the append fused into the attention launch (s2l_append_chunk_prefill_attn:
@@ -257,6 +277,16 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    # spread: four more replays of the same K steps (reported beside, not in, ms_per_step)
+    step_runs = []
+    for _ in range(4):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(main_stream):
+            e0.record(main_stream)
+            timed_graph.replay()
+            e1.record(main_stream)
+        torch.cuda.synchronize()
+        step_runs.append(e0.elapsed_time(e1) / args.steps)
     fused_ms = None
     if fused_graph is not None:
         with torch.cuda.stream(main_stream):
@@ -271,7 +301,7 @@ def main():
     # timed region 2: each kernel alone, L launches back to back per replay (average launch
     # duration, HIP events on the stream the kernels run on)
     per_kernel = {}
-    reps = max(1, args.steps // L + 1)
+    reps = 10
     with torch.cuda.stream(main_stream):
         for name, g in kernel_graphs.items():
             g.replay()
@@ -285,7 +315,8 @@ def main():
             torch.cuda.synchronize()
             per_kernel[name] = [x.elapsed_time(y) / L for x, y in times]
     main_ms = float(np.mean(per_kernel["attn_main"]))
-    step_breakdown = {k: round(float(np.mean(v)) * 1e3, 2) for k, v in per_kernel.items()}
+    step_breakdown = {k: round(float(np.median(v)) * 1e3, 2) for k, v in per_kernel.items()}
+    step_spread = {k: [round(float(np.percentile(v, q)) * 1e3, 2) for q in (10, 90)] for k, v in per_kernel.items()}
     # the step's outputs come from the graphs: check that the last replay left finite values
     assert torch.isfinite(out.float()).all(), "non-finite attention output"
 
@@ -316,11 +347,15 @@ def main():
         "us_per_chunk": round(ms_per_layer * 1e3, 2),
         "pct_mfma_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
         "step_breakdown_us": step_breakdown,
+        "step_breakdown_p10_p90_us": step_spread,
+        "ms_per_step_more_runs": [round(x, 5) for x in step_runs],
         "step_structure": f"plan once per step, then {L} x (append, attention, split merge); step_breakdown_us "
                           f"gives each kernel's average launch",
         "timing": ("direct launches (--eager)" if args.eager else
-                   "one HIP graph of the K steps, replayed once; per-kernel times are averages over "
-                   "graphs of back-to-back launches of that kernel"),
+                   "one HIP graph of the K steps, replayed once (ms_per_step), then four more times "
+                   "(ms_per_step_more_runs); per-kernel times: median (p10, p90) over 10 replays of a "
+                   "graph of 32 back-to-back launches of that kernel; attn_main_warm re-reads one "
+                   "layer's pool (cache-resident), attn_main rotates over the 32 layers' pools"),
         "plan": {"work_items": plan.num_items, "split_requests": plan.num_split_reqs,
                  "split_keys": plan.split_keys, "tile_cols": plan.tile_cols, "key_halves": plan.key_halves},
         "wall_s_timed_region": round(wall, 4),
