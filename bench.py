@@ -350,7 +350,7 @@ def main():
         "step_breakdown_p10_p90_us": step_spread,
         "ms_per_step_more_runs": [round(x, 5) for x in step_runs],
         "step_structure": f"plan once per step, then {L} x (append, attention, split merge); step_breakdown_us "
-                          f"gives each kernel's average launch",
+                          f"gives each kernel's median launch",
         "timing": ("direct launches (--eager)" if args.eager else
                    "one HIP graph of the K steps, replayed once (ms_per_step), then four more times "
                    "(ms_per_step_more_runs); per-kernel times: median (p10, p90) over 10 replays of a "
