@@ -263,6 +263,21 @@ s2l_status s2l_append_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_ba
                                          size_t ws_bytes, int32_t* fused_out, void* stream);
 
 /*
+ * s2l_chunk_prefill_attn (Sec. 2.1 attention over the paged cache) with Q quantised too, for
+ * e4m3 caches: S = Q K^T runs on the fp8 MFMA (v_mfma_f32_32x32x64_f8f6f4) with K's codes
+ * as stored, P V stays on bf16.  Each (token, head) row of Q is encoded as the pages are,
+ * with its own scale s = max|q| / 448 (1 for an all-zero row), inv = 1 / s (both fp32,
+ * correctly rounded), code = e4m3(fp32(q * inv)), round to nearest even, saturating; the
+ * result is the attention of those dequantised rows (code * s) over the dequantised cache,
+ * to the same rounding contract as s2l_chunk_prefill_attn.  Arguments as there.  Returns
+ * S2L_ENOTSUP for a bf16 cache or a plan with 16-column (decode) tiles.  The quantisation is
+ * not in the paper: it is a variant of this library for caches that are already e4m3.
+ */
+s2l_status s2l_chunk_prefill_attn_q8(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q,
+                                     int32_t num_q_heads, float softmax_scale, void* out, float* lse,
+                                     const s2l_plan_info* plan, void* workspace, size_t ws_bytes, void* stream);
+
+/*
  * The main attention kernel alone (online softmax over the work items of the plan).
  * Unsplit requests get their final out/lse; split requests get fp32 partials (unnormalised
  * output, then reference max and running sum) in the workspace, merged by s2l_split_reduce.

@@ -89,3 +89,22 @@ def quantise_kv(x_f32, scale_f32):
     if inv.ndim == 1:
         inv = inv[:, None]                         # broadcast over D for [..][Hkv][D]
     return e4m3_encode(f32_mul(x_f32, inv).astype(np.float64))
+
+
+def quantize_rows(x):
+    """Per-row e4m3 quantisation of float32 rows ``x`` [..., D] (the quantised-Q variant of the
+    attention: each (token, head) row of Q gets its own scale).
+
+    For each row: amax = max |x| (exact); scale = fp32(amax / 448), or 1 for an all-zero row;
+    inv = fp32(1 / scale); codes = e4m3_encode(fp32(x * inv)) (RNE, satfinite).  All fp32
+    operations are single IEEE roundings (numpy float32 arithmetic), as the page encoder's.
+    Returns (codes uint8 [..., D], scale float32 [...], dequantised float64 [..., D] =
+    decode(codes) * scale, exact).
+    """
+    x = np.asarray(x, dtype=np.float32)
+    amax = np.max(np.abs(x), axis=-1)
+    scale = np.where(amax > 0, amax / np.float32(E4M3_MAX), np.float32(1.0)).astype(np.float32)
+    inv = f32_recip(scale)
+    codes = e4m3_encode(f32_mul(x, inv[..., None]).astype(np.float64))
+    deq = e4m3_decode(codes) * scale.astype(np.float64)[..., None]
+    return codes, scale, deq

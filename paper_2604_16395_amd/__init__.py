@@ -25,7 +25,7 @@ from ._lib import (S2L_KV_BF16, S2L_KV_FP8_E4M3, S2LError, S2LLibraryMissing, s2
 __all__ = ["PagedKVCache", "Batch", "plan_opts", "S2LError", "S2LLibraryMissing",
            "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in",
            "s2l_check_tables", "s2l_append_chunk_prefill_attn", "s2l_calib_stream_read", "s2l_calib_mfma_bf16", "s2l_attn_workspace_bytes",
-           "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_attn_main", "s2l_split_reduce",
+           "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_chunk_prefill_attn_q8", "s2l_attn_main", "s2l_split_reduce",
            "s2l_plan_host", "library_path"]
 
 HEAD_DIM = 128
@@ -223,6 +223,14 @@ def _attn(name, cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, wor
 def s2l_chunk_prefill_attn(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace,
                            stream=None):
     _attn("s2l_chunk_prefill_attn", cache, batch, q, num_q_heads, softmax_scale, out, lse, plan,
+          workspace, stream)
+
+
+def s2l_chunk_prefill_attn_q8(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace,
+                              stream=None):
+    """s2l_chunk_prefill_attn with Q quantised to e4m3 per (token, head) row and Q K^T on the
+    fp8 MFMA (e4m3 caches only)."""
+    _attn("s2l_chunk_prefill_attn_q8", cache, batch, q, num_q_heads, softmax_scale, out, lse, plan,
           workspace, stream)
 
 

@@ -93,6 +93,8 @@ SIGNATURES = {
     "s2l_attn_plan": (c_i32, [P_batch, c_i32, c_i32, P_opts, c_vp, ctypes.c_size_t, P_info, c_vp]),
     "s2l_chunk_prefill_attn": (c_i32, [P_cache, P_batch, c_vp, c_i32, ctypes.c_float, c_vp, c_vp, P_info,
                                        c_vp, ctypes.c_size_t, c_vp]),
+    "s2l_chunk_prefill_attn_q8": (c_i32, [P_cache, P_batch, c_vp, c_i32, ctypes.c_float, c_vp, c_vp, P_info,
+                                       c_vp, ctypes.c_size_t, c_vp]),
     "s2l_append_chunk_prefill_attn": (c_i32, [P_cache, P_batch, c_vp, c_vp, c_vp, c_i32, ctypes.c_float, c_vp,
                                               c_vp, P_info, c_vp, ctypes.c_size_t, P_i32, c_vp]),
     "s2l_attn_main": (c_i32, [P_cache, P_batch, c_vp, c_i32, ctypes.c_float, c_vp, c_vp, P_info,

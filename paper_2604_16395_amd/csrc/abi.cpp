@@ -308,7 +308,8 @@ s2l_status attn_common(const s2l_kv_cache* cache, const s2l_batch* batch, const 
 
 s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q, int32_t num_q_heads,
                        float softmax_scale, void* out, float* lse, const s2l_plan_info* plan, void* workspace,
-                       size_t ws_bytes, void* stream, const void* k_new = nullptr, const void* v_new = nullptr) {
+                       size_t ws_bytes, void* stream, const void* k_new = nullptr, const void* v_new = nullptr,
+                       bool q8 = false) {
   int64_t T = 0;
   s2l_status st = attn_common(cache, batch, q, num_q_heads, softmax_scale, out, plan, workspace, ws_bytes, &T);
   if (st != S2L_OK) return st;
@@ -326,6 +327,7 @@ s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const 
   a.group_by_xcd = (plan->flags & S2L_PLAN_UNIFORM) != 0;
   a.knew = k_new;
   a.vnew = v_new;
+  a.q8 = q8;
   (void)hipGetLastError();
   hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("attn_main launch", e);
@@ -583,6 +585,19 @@ s2l_status s2l_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_batch* ba
                                   const s2l_plan_info* plan, void* workspace, size_t ws_bytes, void* stream) {
   s2l_status st = attn_launch(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes,
                               stream);
+  if (st != S2L_OK) return st;
+  return s2l_split_reduce(batch, num_q_heads, out, lse, plan, workspace, ws_bytes, stream);
+}
+
+s2l_status s2l_chunk_prefill_attn_q8(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q,
+                                     int32_t num_q_heads, float softmax_scale, void* out, float* lse,
+                                     const s2l_plan_info* plan, void* workspace, size_t ws_bytes, void* stream) {
+  if (cache && cache->dtype != S2L_KV_FP8_E4M3)
+    return fail(S2L_ENOTSUP, "the quantised-Q path needs an e4m3 cache");
+  if (plan && plan->tile_cols == s2l::kDecodeTileCols)
+    return fail(S2L_ENOTSUP, "the quantised-Q path has no 16-column (decode) tiles: plan with tile_cols 128 or 256");
+  s2l_status st = attn_launch(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, ws_bytes,
+                              stream, nullptr, nullptr, true);
   if (st != S2L_OK) return st;
   return s2l_split_reduce(batch, num_q_heads, out, lse, plan, workspace, ws_bytes, stream);
 }

@@ -158,7 +158,7 @@ struct Ring {
   static constexpr int kBytes = kHalves * kGroupBytes;
 };
 
-template <bool kFp8, int kColWaves, int kHalves, bool kFused>
+template <bool kFp8, int kColWaves, int kHalves, bool kFused, bool kQ8>
 __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)) void attn_main_kernel(
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out, float* __restrict__ lse,
     void* kpool, void* vpool, const float* __restrict__ kscale,
@@ -225,13 +225,46 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
 
   // Q^T operand: lane (n, half) holds Q[col][16 ks + 8 half .. +7] for ks = 0..7.
   bf16x8 qf[8];
-  {
+  // kQ8: the column quantised to e4m3 with its own scale sq = max |Q[col]| / 448 (1 for a
+  // zero column; both divisions correctly rounded, codes RNE with saturation, as the page
+  // encoder); for the fp8 MFMA of k-half j lane (n, half) holds the codes of
+  // Q[col][32 (2 j + half) + b], b < 32, and the scores take sq in their scale.
+  i32x8 q8[2];
+  if constexpr (!kQ8) {
     const uint16_t* qrow = q + ((int64_t)(row0 + (valid ? tok : 0)) * hq + (valid ? hq_col : 0)) * 128 + 8 * half;
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       u32x4 x = valid ? *reinterpret_cast<const u32x4*>(qrow + 16 * ks) : u32x4{0, 0, 0, 0};
       qf[ks] = __builtin_bit_cast(bf16x8, x);
     }
+  } else {
+    const uint16_t* qrow = q + ((int64_t)(row0 + (valid ? tok : 0)) * hq + (valid ? hq_col : 0)) * 128 + 32 * half;
+    u32x4 x[8];   // x[4 j + i]: dims 32 (2 j + half) + 8 i .. + 7
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        x[4 * j + i] = valid ? *reinterpret_cast<const u32x4*>(qrow + 64 * j + 8 * i) : u32x4{0, 0, 0, 0};
+    float amax = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k)
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+        amax = fmaxf(amax, fmaxf(fabsf(u2f(x[k][w] << 16)), fabsf(u2f(x[k][w] & 0xffff0000u))));
+    amax = max_with_partner(amax);
+    const float sq = amax > 0.f ? __fdiv_rn(amax, 448.f) : 1.f;
+    const float inv = __fdiv_rn(1.f, sq);
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const uint32_t w0 = x[4 * j + i][2 * h], w1 = x[4 * j + i][2 * h + 1];
+          q8[j][2 * i + h] = (int)f32x4_to_fp8x4(u2f(w0 << 16) * inv, u2f(w0 & 0xffff0000u) * inv,
+                                                 u2f(w1 << 16) * inv, u2f(w1 & 0xffff0000u) * inv);
+        }
+    c_log2 *= sq;
   }
 
   // LDS byte offsets of the operand reads, relative to a tile buffer.
@@ -239,6 +272,14 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   uint32_t ka[8];
 #pragma unroll
   for (int ks = 0; ks < 8; ++ks) ka[ks] = grp_base + n * kRowBytes + ((((2 * ks + half) ^ (n & 15))) << 4);
+  // kQ8: K stays e4m3 in LDS, the 8 16-byte chunks of a key's codes in the same permuted
+  // positions of its 256-byte row slot (chunk c at c ^ (r & 15)); the fp8 MFMA of k-half j
+  // reads chunks 4 j + 2 half and 4 j + 2 half + 1 of row n.
+  uint32_t ka8[2][2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int t = 0; t < 2; ++t) ka8[j][t] = grp_base + n * kRowBytes + (((4 * j + 2 * half + t) ^ (n & 15)) << 4);
   // V^T (A of O^T += V^T P^T), d-block db, first 4-key set of k-step 0: within each group
   // of 16 lanes, lane j addresses key row (j >> 2) at column 32 db + 16 ((l >> 4) & 1) +
   // 4 (j & 3); the transposing read hands lane i the four keys of column base + i, so lane
@@ -267,6 +308,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   // copied straight from the new K/V rows (row stride hkv * 256 bytes) instead of the pages,
   // which this same launch writes; kno / vno are the lane offsets for that source.
   static_assert(!(kFp8 && kFused), "the fused append is for bf16 pages");
+  static_assert(!kQ8 || kFp8, "Q is quantised only against e4m3 pages");
   const uint32_t new_stride = (uint32_t)hkv * kRowBytes;
   uint32_t kno[kFp8 ? 1 : kDma], vno[kFp8 ? 1 : kDma];
   if constexpr (!kFp8) {
@@ -360,6 +402,10 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     for (int i = 0; i < kF8Loads; ++i) {
       constexpr int kLpr = 8 / kF8Loads;
       const int row = 16 * pw + s0 + lane / kLpr, f = (lane % kLpr) * kF8Loads + i;
+      if (kQ8 && is_k) {   // the codes as they are, chunk f at f ^ (row & 15)
+        *reinterpret_cast<u32x4*>(smem + grp_base + dst + row * kRowBytes + ((f ^ (row & 15)) << 4)) = st.x[i];
+        continue;
+      }
       const int sw = is_k ? (row & 15) : ((row & 3) << 2);
       const u32x2 a = fp8x4_to_bf16x4(st.x[i][0]);
       const u32x2 b = fp8x4_to_bf16x4(st.x[i][1]);
@@ -377,13 +423,28 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   float m_run = 0.f;
   float l_run = 0.f;   // sum of the bf16 probabilities exactly as P.V uses them
 
+  // kQ8: the e4m3 codes of K for the fp8 MFMA of k-half j, sub-block at LDS byte `kofs`.
+  auto read_k8 = [&](int kofs, int j) {
+    const u32x4 lo = *reinterpret_cast<const u32x4*>(smem + kofs + ka8[j][0]);
+    const u32x4 hi = *reinterpret_cast<const u32x4*>(smem + kofs + ka8[j][1]);
+    return i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+  };
+  // S^T += K Q^T over 64 dims in e4m3 (both operands' codes; their scales are in c_log2)
+  auto mfma_q8 = [&](const i32x8& a, const i32x8& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+  };
   // S(b+1) = K(b+1) Q^T from the sub-block at LDS byte `kofs`.
   auto qk = [&](int kofs) {
     f32x16 s = f32x16{};
+    if constexpr (kQ8) {
+      s = mfma_q8(read_k8(kofs, 0), q8[0], s);
+      s = mfma_q8(read_k8(kofs, 1), q8[1], s);
+    } else {
 #pragma unroll
-    for (int ks = 0; ks < 8; ++ks) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(smem + kofs + ka[ks]);
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s, 0, 0, 0);
+      for (int ks = 0; ks < 8; ++ks) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8*>(smem + kofs + ka[ks]);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], s, 0, 0, 0);
+      }
     }
     return s;
   };
@@ -408,12 +469,18 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   // Operands of a step's first two slots, read before its (branchy) softmax prologue.
   struct Pre {
     bf16x8 k[2], v[2];
+    i32x8 k8[2];   // kQ8: both fp8 K operands of the step
   };
   auto prefetch = [&](int kofs, int vofs, auto with_qk) {
     Pre f;
     if constexpr (decltype(with_qk)::value) {
-      f.k[0] = read_k(kofs, 0);
-      f.k[1] = read_k(kofs, 1);
+      if constexpr (kQ8) {
+        f.k8[0] = read_k8(kofs, 0);
+        f.k8[1] = read_k8(kofs, 1);
+      } else {
+        f.k[0] = read_k(kofs, 0);
+        f.k[1] = read_k(kofs, 1);
+      }
     }
     f.v[0] = read_v(vofs, 0, 0);
     f.v[1] = read_v(vofs, 0, 1);
@@ -438,13 +505,18 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       if (i + 2 < 8) {
-        if constexpr (kQK) kf[i + 2] = read_k(kofs, i + 2);
+        if constexpr (kQK && !kQ8) kf[i + 2] = read_k(kofs, i + 2);
         vf[i + 2] = read_v(vofs, (i + 2) >> 2, (i + 2) & 3);
       } else if constexpr (kNext) {
-        nxt.k[i - 6] = read_k(nkofs, i - 6);
+        if constexpr (kQ8) nxt.k8[i - 6] = read_k8(nkofs, i - 6);
+        else nxt.k[i - 6] = read_k(nkofs, i - 6);
         nxt.v[i - 6] = read_v(nvofs, 0, i - 6);
       }
-      if constexpr (kQK) sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i], qf[i], sn, 0, 0, 0);
+      if constexpr (kQK && kQ8) {
+        if (i < 2) sn = mfma_q8(f.k8[i], q8[i], sn);   // the two fp8 MFMAs in the first slots
+      } else if constexpr (kQK) {
+        sn = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i], qf[i], sn, 0, 0, 0);
+      }
       o[i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i], __builtin_bit_cast(bf16x8, pp[i >> 2]), o[i & 3],
                                                           0, 0, 0);
       const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[2 * i], c_log2, -m_run));
@@ -457,14 +529,16 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     }
     lsum = l0 + l1;
     __asm__ volatile("" ::"v"(po[0]), "v"(po[1]), "v"(lsum));   // produced here, not sunk
-    slot_schedule<kQK, true>();
-    slot_schedule<kQK, true>();
-    slot_schedule<kQK, true>();
-    slot_schedule<kQK, true>();
-    slot_schedule<kQK, true>();
-    slot_schedule<kQK, true>();
-    slot_schedule<kQK, kNext>();
-    slot_schedule<kQK, kNext>();
+    if constexpr (!kQ8) {
+      slot_schedule<kQK, true>();
+      slot_schedule<kQK, true>();
+      slot_schedule<kQK, true>();
+      slot_schedule<kQK, true>();
+      slot_schedule<kQK, true>();
+      slot_schedule<kQK, true>();
+      slot_schedule<kQK, kNext>();
+      slot_schedule<kQK, kNext>();
+    }
     return sn;
   };
   // Mask of sub-block sb0 (element e of a lane's scores is key sb0 + 8 (e / 4) + 4 half +
@@ -859,9 +933,9 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(uint16_t* __restrict_
 
 }  // namespace
 
-template <bool kFp8, int kColWaves, int kHalves, bool kFused>
+template <bool kFp8, int kColWaves, int kHalves, bool kFused, bool kQ8 = false>
 void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
-  attn_main_kernel<kFp8, kColWaves, kHalves, kFused><<<(unsigned)a.dims.num_items, kColWaves * kHalves * 64, 0, stream>>>(
+  attn_main_kernel<kFp8, kColWaves, kHalves, kFused, kQ8><<<(unsigned)a.dims.num_items, kColWaves * kHalves * 64, 0, stream>>>(
       static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
       a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, a.softmax_scale * kLog2e,
       plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0, static_cast<const uint16_t*>(a.knew),
@@ -876,6 +950,13 @@ void launch_main_dtype(const AttnLaunch& a, hipStream_t stream) {
     if (a.tile_cols == kMaxTileCols) launch_main_variant<false, 8, 1, true>(a, stream);
     else if (a.key_halves == 2) launch_main_variant<false, 4, 2, true>(a, stream);
     else launch_main_variant<false, 4, 1, true>(a, stream);
+    return;
+  }
+  if (kFp8 && a.q8) {
+    // Q quantised to e4m3 and S = Q K^T on the fp8 MFMA (e4m3 pages only)
+    if (a.tile_cols == kMaxTileCols) launch_main_variant<true, 8, 1, false, true>(a, stream);
+    else if (a.key_halves == 2) launch_main_variant<true, 4, 2, false, true>(a, stream);
+    else launch_main_variant<true, 4, 1, false, true>(a, stream);
     return;
   }
   if (a.tile_cols == kMaxTileCols) launch_main_variant<kFp8, 8, 1, kF>(a, stream);

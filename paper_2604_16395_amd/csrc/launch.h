@@ -73,6 +73,7 @@ struct AttnLaunch {
   bool group_by_xcd;        // items of near-equal cost: consecutive items onto one XCD
   const void* knew = nullptr;   // fused append (bf16, page-aligned prefixes): the chunk's
   const void* vnew = nullptr;   //   new K/V rows [T][Hkv][128], else null
+  bool q8 = false;              // e4m3 pages: Q quantised per column, S on the fp8 MFMA
 };
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream);
 

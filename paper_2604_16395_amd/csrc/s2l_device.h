@@ -12,6 +12,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef int i32x8 __attribute__((ext_vector_type(8)));
 
 __device__ inline uint32_t f2u(float x) { return __builtin_bit_cast(uint32_t, x); }
 __device__ inline float u2f(uint32_t x) { return __builtin_bit_cast(float, x); }

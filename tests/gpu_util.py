@@ -7,6 +7,7 @@ import torch
 
 import paper_2604_16395_amd as s2l
 from oracle.attention import ref_batch_attn
+from oracle.fp8_e4m3 import quantize_rows
 from oracle.paged_kv import bf16_bits_to_f32, ref_append
 from workloads import BF16_SENTINEL, FP8_SENTINEL
 
@@ -85,7 +86,7 @@ class Setup:
                    self.case.v_scale)
         self.appended = True
 
-    def attention(self, opts=None, with_lse=True, use_main_and_reduce=False):
+    def attention(self, opts=None, with_lse=True, use_main_and_reduce=False, q8=False):
         c = self.case
         T, hq = c.total_tokens, c.num_q_heads
         nbytes = s2l.s2l_attn_workspace_bytes(self.batch, hq, c.num_kv_heads, opts)
@@ -93,7 +94,9 @@ class Setup:
         plan = s2l.s2l_attn_plan(self.batch, hq, c.num_kv_heads, ws, opts)
         out = torch.full((T, hq, 128), float("nan"), dtype=torch.bfloat16, device=DEV)
         lse = torch.full((T, hq), float("nan"), dtype=torch.float32, device=DEV) if with_lse else None
-        if use_main_and_reduce:
+        if q8:
+            s2l.s2l_chunk_prefill_attn_q8(self.cache, self.batch, self.q, hq, SCALE, out, lse, plan, ws)
+        elif use_main_and_reduce:
             s2l.s2l_attn_main(self.cache, self.batch, self.q, hq, SCALE, out, lse, plan, ws)
             s2l.s2l_split_reduce(self.batch, hq, out, lse, plan, ws)
         else:
@@ -102,11 +105,13 @@ class Setup:
         self.plan = plan
         return out, lse
 
-    def oracle(self, sample_rows=None):
+    def oracle(self, sample_rows=None, q8=False):
         """(O, LSE, A, B): the oracle's output, log-sum-exp and the softmax-weighted means of
-        |V| and of |V - O|."""
+        |V| and of |V - O|.  q8: of the queries quantised per (token, head) row to e4m3."""
         c = self.case
         q = bf16_bits_to_f32(c.q_bits).astype(np.float64)
+        if q8:
+            q = quantize_rows(bf16_bits_to_f32(c.q_bits))[2]
         return ref_batch_attn(q, self.kp_ref, self.vp_ref, self.tables, c.prefix_lens, c.chunk_lens,
                               c.cu_chunk, c.num_q_heads, SCALE, c.kv_dtype, c.k_scale, c.v_scale,
                               sample_rows=sample_rows, with_abs=True)

@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 import torch
 
-from oracle.fp8_e4m3 import e4m3_decode, e4m3_encode, quantise_kv
+from oracle.fp8_e4m3 import e4m3_decode, e4m3_encode, quantise_kv, quantize_rows
 
 GOLD = os.path.join(os.path.dirname(__file__), "golden", "ocp_e4m3_named_values.json")
 ALL = np.arange(256, dtype=np.uint8)
@@ -103,3 +103,53 @@ def test_quantise_with_power_of_two_and_generic_scale(scale):
     if scale in (0.25, 2.0 ** -7):
         # power-of-two scale: the product is exact, so decode*scale equals RNE(x) exactly
         assert np.allclose(dec * scale, e4m3_decode(e4m3_encode(x / scale)) * scale, rtol=0, atol=0)
+
+
+# --- per-row quantisation of Q (the quantised-Q attention variant) ---------------------------
+
+def test_rows_of_exact_codes_with_a_power_of_two_scale_round_trip():
+    """A row made of e4m3 values times 2^k whose largest magnitude is 448 * 2^k has scale
+    2^k exactly, so every element comes back unchanged."""
+    rng = np.random.default_rng(11)
+    finite = ALL[(ALL & 0x7F) != 0x7F]
+    for k in (-9, -3, 0, 2):
+        codes = rng.choice(finite, size=(6, 128))
+        codes[:, 5] = 0x7E                               # +448 in every row
+        x = (e4m3_decode(codes) * 2.0 ** k).astype(np.float32)
+        c, s, d = quantize_rows(x)
+        assert np.all(s == np.float32(2.0 ** k))
+        assert np.array_equal(d, x.astype(np.float64))
+
+
+def test_row_quantisation_error_within_the_e4m3_bound():
+    """Round to nearest in E4M3: within half a quantum, i.e. 2^-4 relative in the normal range
+    (scaled |x| >= 2^-6) and 2^-10 absolute (times the scale) below it; the fp32 product
+    before rounding adds at most 2^-23 relative."""
+    rng = np.random.default_rng(12)
+    x = (rng.standard_normal((64, 128)) * rng.choice([0.01, 0.5, 30.0], size=(64, 1))).astype(np.float32)
+    x[3, :] = np.float32(0.0)
+    x[4, 7] = np.float32(1e-3)                           # one tiny element among zeros
+    x[4, :7] = 0
+    x[4, 8:] = 0
+    c, s, d = quantize_rows(x)
+    xs = np.abs(x.astype(np.float64)) / s[:, None]
+    err = np.abs(d - x.astype(np.float64)) / s[:, None]
+    normal = xs >= 2.0 ** -6
+    assert np.all(err[normal] <= (2.0 ** -4 + 2.0 ** -22) * xs[normal])
+    assert np.all(err[~normal] <= 2.0 ** -10 + 2.0 ** -22 * xs[~normal])
+    # the largest element of a non-zero row is 448 * scale (code 0x7E or 0xFE); a zero row
+    # has scale 1 and zero codes
+    nz = np.abs(x).max(axis=1) > 0
+    amax_idx = np.abs(x).argmax(axis=1)
+    assert np.all((c[np.arange(64), amax_idx][nz] & 0x7F) == 0x7E)
+    assert s[3] == 1.0 and not c[3].any() and not d[3].any()
+
+
+def test_row_quantisation_is_odd_and_commutes_with_powers_of_two():
+    rng = np.random.default_rng(13)
+    x = (rng.standard_normal((8, 128)) * 0.5).astype(np.float32)
+    c, s, d = quantize_rows(x)
+    cn, sn, dn = quantize_rows(-x)
+    assert np.array_equal(cn, c ^ 0x80) and np.array_equal(sn, s) and np.array_equal(dn, -d)
+    c4, s4, d4 = quantize_rows(x * np.float32(16.0))
+    assert np.array_equal(c4, c) and np.array_equal(s4, s * np.float32(16.0)) and np.array_equal(d4, 16.0 * d)
