@@ -239,12 +239,20 @@ def cfg5(stream, gen):
     layer = Layer(P, C, 64, 8, 10400, tables_for(P, C, 10400, rng), gen, fp8=True, copies=2)
     us, attn_us, plan = measure_step(layer, stream, 2, reps=3)
     f = layer.flops()
+    # the quantised-Q variant on the same layer (Q rows to e4m3, Q K^T on the fp8 MFMA)
+    q8_ms = timed_graph(lambda: [s2l.s2l_chunk_prefill_attn_q8(layer.caches[i], layer.batch, layer.q, 64, SCALE,
+                                                               layer.out, layer.lse, plan, layer.ws, stream)
+                                 for i in range(2)], stream, reps=3) / 2
     return {"workload": "Llama-3-70B layer share: P = 131072, C = 2048, 64q/8kv, fp8 E4M3 KV with per-head "
                         "scales, 2 rotating layer copies",
             "ms_per_step": round(us / 1e3, 3), "attn_ms": round(attn_us / 1e3, 3),
             "attn_tflops": round(f / attn_us / 1e6, 1),
             "attn_pct_mfma_peak": round(100 * f / attn_us / 1e6 / PEAK_BF16_TFLOPS, 1),
-            "work_items": plan.num_items, "tile_cols": plan.tile_cols}
+            "work_items": plan.num_items, "tile_cols": plan.tile_cols,
+            "quantised_q": {"what": "s2l_chunk_prefill_attn_q8: Q rows quantised to e4m3, Q K^T on the fp8 MFMA, "
+                                    "P V on bf16 (no split here, so this is the attention launch)",
+                            "ms": round(q8_ms, 3), "tflops": round(f / q8_ms / 1e9, 1),
+                            "pct_bf16_mfma_peak": round(100 * f / q8_ms / 1e9 / PEAK_BF16_TFLOPS, 1)}}
 
 
 def scheduler_latency(seed=2024, sizes=(50, 500), calls=2000):
