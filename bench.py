@@ -194,7 +194,7 @@ def main():
     # graph: the cross-stream dependencies cost more than the overlap saves.)
     plan_box = {}
 
-    def enqueue_step(_=None):
+    def enqueue_step():
         plan_box["plan"] = s2l.s2l_attn_plan(batch, HQ, HKV, ws, opts, main_stream)
         for l in range(L):
             s2l.s2l_kv_append(caches[l], batch, k_new, v_new, main_stream)
@@ -220,7 +220,7 @@ def main():
         return g
 
     with torch.cuda.stream(main_stream):
-        enqueue_step(0)          # eager run: the plan exists before any single-kernel graph
+        enqueue_step()           # eager run: the plan exists before any single-kernel graph
     torch.cuda.synchronize()
     plan = plan_box["plan"]
     # the warm-up steps and the K timed steps, one graph each (steps rotate over the layer copies)
