@@ -104,6 +104,26 @@ def cpu_baseline(case, min_seconds=10.0, max_reps=5):
                            "sample": f"every 8th chunk row ({len(rows[0])} rows x 32 heads), {e1:.1f} s"}
     except ImportError:
         pass
+    # the small configuration (one request, P=256, C=128, 8q/2kv) with both oracle forms: the
+    # per-row loops and the blocked form
+    c1 = workloads.config1()
+    shape1 = (c1.num_pages, c1.num_kv_heads, 16, 128)
+    kp1 = np.full(shape1, workloads.BF16_SENTINEL, np.uint16)
+    vp1 = np.full(shape1, workloads.BF16_SENTINEL, np.uint16)
+    seq1 = (c1.prefix_lens + c1.chunk_lens).astype(np.int32)
+    cu1 = np.zeros(c1.num_reqs + 1, np.int32)
+    cu1[1:] = np.cumsum(seq1)
+    ref_append(kp1, vp1, c1.block_tables, np.zeros(c1.num_reqs, np.int32), seq1, cu1, c1.k_full_bits, c1.v_full_bits)
+    q1 = bf16_bits_to_f32(c1.q_bits).astype(np.float64)
+    f1 = wl.attn_flops(c1.prefix_lens, c1.chunk_lens, c1.num_q_heads)
+    res["config1"] = {"unit": "TFLOP/s"}
+    for method in ("loops", "blocked"):
+        t1 = time.perf_counter()
+        ref_batch_attn(q1, kp1, vp1, c1.block_tables, c1.prefix_lens, c1.chunk_lens, c1.cu_chunk,
+                       c1.num_q_heads, 1.0 / np.sqrt(128.0), method=method)
+        e1 = time.perf_counter() - t1
+        res["config1"][method] = {"value": f1 / e1 / 1e12, "seconds": round(e1, 3)}
+    res["config1"]["sample"] = "whole config 1 (P=256, C=128, 8q/2kv), once per oracle form"
     return res
 
 
