@@ -106,3 +106,38 @@ def test_streaming_64_chunks_equals_one_shot_prefill():
     vmax_q = np.repeat(vmax, 4)[None, :, None]                   # query head h reads kv head h // 4
     u = 2.0 ** -8
     assert (np.abs(a - b) <= 2 * u * 1.01 * np.abs(b) + 8.1 * u * vmax_q + 2 ** -15 * vmax_q + 2e-6).all()
+
+
+def test_back_to_back_launches_are_bit_identical():
+    """Sustained launches of the 8K-prefix step's attention (256 items, the four-stage copy
+    ring), of the fused append + attention and of the quantised-Q path, queued without host
+    synchronisation: every output equals the first bit for bit."""
+    case = workloads.make_case("b2b", [8192], [512], 32, 8, seed=26)
+    s = Setup(case)
+    s.append()
+    c = case
+    ws = torch.empty(s2l.s2l_attn_workspace_bytes(s.batch, 32, 8), dtype=torch.uint8, device=DEV)
+    plan = s2l.s2l_attn_plan(s.batch, 32, 8, ws)
+    assert plan.num_items == 256
+    outs = [torch.empty((512, 32, 128), dtype=torch.bfloat16, device=DEV) for _ in range(40)]
+    lses = [torch.empty((512, 32), dtype=torch.float32, device=DEV) for _ in range(40)]
+    for o, l in zip(outs, lses):
+        s2l.s2l_chunk_prefill_attn(s.cache, s.batch, s.q, 32, SCALE, o, l, plan, ws)
+    torch.cuda.synchronize()
+    assert all(_eq(outs[0], o) and torch.equal(lses[0], l) for o, l in zip(outs[1:], lses[1:]))
+    # fused: the pages already hold the chunk, and rewriting them with the same rows is a no-op
+    k_new, v_new = to_bf16(s.k_new), to_bf16(s.v_new)
+    for o, l in zip(outs, lses):
+        assert s2l.s2l_append_chunk_prefill_attn(s.cache, s.batch, k_new, v_new, s.q, 32, SCALE, o, l, plan, ws)
+    torch.cuda.synchronize()
+    assert all(_eq(outs[0], o) and torch.equal(lses[0], l) for o, l in zip(outs[1:], lses[1:]))
+    f8 = workloads.make_case("b2b8", [16384], [512], 64, 8, seed=27, kv_dtype="fp8")
+    s8 = Setup(f8)
+    s8.append()
+    ws8 = torch.empty(s2l.s2l_attn_workspace_bytes(s8.batch, 64, 8), dtype=torch.uint8, device=DEV)
+    plan8 = s2l.s2l_attn_plan(s8.batch, 64, 8, ws8)
+    o8 = [torch.empty((512, 64, 128), dtype=torch.bfloat16, device=DEV) for _ in range(20)]
+    for o in o8:
+        s2l.s2l_chunk_prefill_attn_q8(s8.cache, s8.batch, s8.q, 64, SCALE, o, None, plan8, ws8)
+    torch.cuda.synchronize()
+    assert all(_eq(o8[0], o) for o in o8[1:])
