@@ -35,9 +35,15 @@ KERNEL_SOURCES = ["paper_2604_16395_amd/csrc/chunk_attn.hip", "paper_2604_16395_
 
 
 def kernel_source_hash():
+    """Hash of the kernel sources with comments and blank lines removed, so that a counter
+    summary stays attached to the code it measured across comment-only edits."""
     h = hashlib.sha256()
     for p in KERNEL_SOURCES:
-        h.update(open(os.path.join(ROOT, p), "rb").read())
+        text = open(os.path.join(ROOT, p)).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", "", text)
+        text = "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+        h.update(text.encode())
     return h.hexdigest()[:16]
 
 

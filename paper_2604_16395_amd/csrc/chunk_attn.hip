@@ -43,6 +43,10 @@
 // overflow at the start of step b, before it enters O.  The causal mask is applied only to
 // sub-blocks that reach past the first query token's position.
 //
+// Quantised-Q variant (e4m3 pages only): each lane pair encodes its column of Q to e4m3 with
+// the column's own scale, K's codes stay e4m3 in LDS (same permuted chunk positions), and the
+// two MFMAs of a step's S are v_mfma_f32_32x32x64_f8f6f4 (64 dims each); P V is unchanged.
+//
 // Unsplit items write bf16 O = acc / l (and LSE).  Split items write fp32 partials
 // (acc, m, l) that split_reduce_kernel merges (log-sum-exp merge of Sec. 2.1's softmax).
 #include "launch.h"
