@@ -7,7 +7,7 @@ import torch
 
 import paper_2604_16395_amd as s2l
 import workloads
-from tests.gpu_util import DEV, SCALE, Setup, assert_attention_close, bf16_to_f64, sample_rows
+from tests.gpu_util import DEV, SCALE, Setup, assert_attention_close, bf16_to_f64, sample_rows, to_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -64,3 +64,38 @@ def test_q8_rejects_bf16_cache_and_decode_tiles():
     s.append()
     with pytest.raises(s2l.S2LError, match="decode"):
         s.attention(s2l.plan_opts(), q8=True)      # C * G = 4 columns: automatic 16-column tiles
+
+
+def test_q8_streamed_chunks_equal_one_shot():
+    """The quantised-Q path keeps the streaming invariant: a 4096-token context arriving as 16
+    chunks of 256 into an e4m3 cache, each chunk attended with quantised Q over the growing
+    prefix, matches the oracle of the quantised queries on sampled rows and the GPU's one-shot
+    quantised-Q run (within twice the bound) on every row.  (Q is quantised per row, so the
+    chunking does not change what is computed.)"""
+    case = workloads.make_case("q8stream", [0], [4096], 32, 8, seed=28, kv_dtype="fp8")
+    s = Setup(case)
+    kp = s.cache.k_pages.clone()                 # the sentinel-filled pools, before any append
+    vp = s.cache.v_pages.clone()
+    s.append()                                   # the whole sequence in the pages (the oracle's view)
+    one, _ = s.attention(q8=True)
+    cache = s2l.PagedKVCache(kp, vp, s.k_scale, s.v_scale)
+    k_all, v_all = to_bf16(s.k_new), to_bf16(s.v_new)
+    out = torch.empty((4096, 32, 128), dtype=torch.bfloat16, device=DEV)
+    for step in range(16):
+        P = 256 * step
+        b = s2l.Batch([P], [256], case.block_tables)
+        s2l.s2l_kv_append(cache, b, k_all[P:P + 256].contiguous(), v_all[P:P + 256].contiguous())
+        ws = torch.empty(s2l.s2l_attn_workspace_bytes(b, 32, 8), dtype=torch.uint8, device=DEV)
+        plan = s2l.s2l_attn_plan(b, 32, 8, ws)
+        s2l.s2l_chunk_prefill_attn_q8(cache, b, s.q[P:P + 256].contiguous(), 32, SCALE, out[P:P + 256], None,
+                                      plan, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(kp, s.cache.k_pages) and torch.equal(vp, s.cache.v_pages)   # same pages either way
+    rows = {0: sorted(set(np.random.default_rng(29).integers(0, 4096, size=96).tolist()) | {0, 255, 256, 4095})}
+    ref = s.oracle(rows, q8=True)
+    assert_attention_close(case, out, None, ref, rows, what="q8 stream")
+    a, b = bf16_to_f64(out), bf16_to_f64(one)
+    vmax = np.abs(bf16_to_f64(v_all)).max(axis=(0, 2))
+    vmax_q = np.repeat(vmax, 4)[None, :, None]
+    u = 2.0 ** -8
+    assert (np.abs(a - b) <= 2 * u * 1.01 * np.abs(b) + 8.1 * u * vmax_q + 2 ** -15 * vmax_q + 2e-6).all()
