@@ -69,8 +69,10 @@ def e4m3_encode(y):
 
 
 def f32_mul(x, s):
-    """float32 product (IEEE RNE) of float32 operands, returned as float32."""
-    return (np.asarray(x, dtype=np.float32) * np.asarray(s, dtype=np.float32)).astype(np.float32)
+    """float32 product (IEEE RNE) of float32 operands, returned as float32.  A product past
+    the float32 range is +-inf, as in IEEE arithmetic (the encoder then saturates it)."""
+    with np.errstate(over="ignore"):
+        return (np.asarray(x, dtype=np.float32) * np.asarray(s, dtype=np.float32)).astype(np.float32)
 
 
 def f32_recip(s):
