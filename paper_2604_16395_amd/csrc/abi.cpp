@@ -563,11 +563,14 @@ s2l_status s2l_append_chunk_prefill_attn(const s2l_kv_cache* cache, const s2l_ba
                                          size_t ws_bytes, int32_t* fused_out, void* stream) {
   s2l_status st;
   int64_t T = 0;
-  if ((st = check_cache(cache, batch)) != S2L_OK) return st;
-  if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
+  // Every argument of both halves is checked before anything is enqueued.
+  if ((st = attn_common(cache, batch, q, num_q_heads, softmax_scale, out, plan, workspace, ws_bytes, &T)) != S2L_OK)
+    return st;
   if (T > 0 && (!k_new || !v_new)) return fail(S2L_EINVAL, "k_new/v_new is NULL");
-  bool fuse = cache->dtype == S2L_KV_BF16 && plan && plan->tile_cols != s2l::kDecodeTileCols;
+  bool fuse = cache->dtype == S2L_KV_BF16 && plan->tile_cols != s2l::kDecodeTileCols;
   for (int32_t r = 0; r < batch->num_reqs && fuse; ++r) fuse = batch->prefix_lens_host[r] % s2l::kPageSize == 0;
+  if (!fuse && (batch->num_reqs > 65535 || cache->num_kv_heads > 65535))
+    return fail(S2L_ENOTSUP, "kv_append supports at most 65535 requests and kv heads");
   if (fused_out) *fused_out = fuse ? 1 : 0;
   if (!fuse) {
     if ((st = s2l_kv_append(cache, batch, k_new, v_new, stream)) != S2L_OK) return st;

@@ -171,3 +171,27 @@ def test_last_error_is_cleared_by_success():
     assert _status("s2l_attn_workspace_bytes", ctypes.byref(b), 8, 3, ctypes.byref(opts), ctypes.byref(n))[1]
     st, msg = _status("s2l_attn_workspace_bytes", ctypes.byref(b), 8, 2, ctypes.byref(opts), ctypes.byref(n))
     assert st == 0 and msg == "" and n.value > 0
+
+
+def test_append_and_attention_checks_every_argument_before_enqueueing():
+    """The two-call fallback (P not a multiple of 16) must not enqueue the append when the
+    attention half is invalid: the call fails with EINVAL or EWORKSPACE from the host checks
+    (an enqueued launch would have reached HIP here, where there is no device, and failed
+    with EHIP instead)."""
+    b, keep = _batch([30], [40])
+    c = _cache(hkv=2)
+    info = _plan([30], [40], 8, 2)
+    ok_bytes = info.workspace_bytes
+    fused = ctypes.c_int32(-1)
+
+    def call(hq=8, scale=0.1, plan=ctypes.byref(info), q=FAKE, nbytes=ok_bytes, kn=FAKE):
+        return _status("s2l_append_chunk_prefill_attn", ctypes.byref(c), ctypes.byref(b), kn, FAKE, q, hq, scale,
+                       FAKE, None, plan, FAKE, nbytes, ctypes.byref(fused), None)[0]
+
+    assert call(hq=16) == _lib.S2L_EINVAL
+    assert call(scale=0.0) == _lib.S2L_EINVAL
+    assert call(plan=None) == _lib.S2L_EINVAL
+    assert call(q=None) == _lib.S2L_EINVAL
+    assert call(kn=None) == _lib.S2L_EINVAL
+    assert call(nbytes=ok_bytes - 1) == _lib.S2L_EWORKSPACE
+    assert fused.value == -1                       # nothing decided, nothing enqueued
