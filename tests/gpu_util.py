@@ -9,6 +9,7 @@ import paper_2604_16395_amd as s2l
 from oracle.attention import ref_batch_attn
 from oracle.fp8_e4m3 import quantize_rows
 from oracle.paged_kv import bf16_bits_to_f32, ref_append
+import workloads
 from workloads import BF16_SENTINEL, FP8_SENTINEL
 
 DEV = "cuda"
@@ -25,6 +26,20 @@ def from_bf16(t):
 
 def bf16_to_f64(t):
     return bf16_bits_to_f32(from_bf16(t)).astype(np.float64)
+
+
+_NAMED = {}
+_PREFIX_POOLS = {}
+_ORACLE = {}
+
+
+def named_case(name):
+    """The named workload ``workloads.<name>()``, drawn once per test session: drawing the large
+    ones (and paging their prefixes into the reference pools) takes tens of seconds on the host.
+    Tests only read the returned case."""
+    if name not in _NAMED:
+        _NAMED[name] = getattr(workloads, name)()
+    return _NAMED[name]
 
 
 def sentinel_pools(case):
@@ -53,12 +68,18 @@ class Setup:
     def __init__(self, case, block_tables=None, prefix_on_gpu=False):
         self.case = case
         self.tables = case.block_tables if block_tables is None else block_tables
+        self.named = block_tables is None and _NAMED.get(case.name) is case
         R = case.num_reqs
-        self.kp_ref, self.vp_ref = sentinel_pools(case)
         zeros = np.zeros(R, np.int32)
         cu_pre = np.zeros(R + 1, np.int32)
         cu_pre[1:] = np.cumsum(case.prefix_lens)
-        pre_k, pre_v = case.prefix_rows(case.k_full_bits), case.prefix_rows(case.v_full_bits)
+        # a named case with its own tables pages its prefix into the reference pools once
+        memo = self.named and not prefix_on_gpu
+        if memo and case.name in _PREFIX_POOLS:
+            self.kp_ref, self.vp_ref = (a.copy() for a in _PREFIX_POOLS[case.name])
+        else:
+            self.kp_ref, self.vp_ref = sentinel_pools(case)
+            pre_k, pre_v = case.prefix_rows(case.k_full_bits), case.prefix_rows(case.v_full_bits)
         self.fp8 = case.kv_dtype == "fp8"
         self.k_scale = None if not self.fp8 else torch.from_numpy(case.k_scale).to(DEV)
         self.v_scale = None if not self.fp8 else torch.from_numpy(case.v_scale).to(DEV)
@@ -68,8 +89,11 @@ class Setup:
             pb = s2l.Batch(zeros, case.prefix_lens, self.tables)
             if len(pre_k):
                 s2l.s2l_kv_append(self.cache, pb, to_bf16(pre_k), to_bf16(pre_v))
-        ref_append(self.kp_ref, self.vp_ref, self.tables, zeros, case.prefix_lens, cu_pre, pre_k, pre_v,
-                   case.kv_dtype, case.k_scale, case.v_scale)
+        if not (memo and case.name in _PREFIX_POOLS):
+            ref_append(self.kp_ref, self.vp_ref, self.tables, zeros, case.prefix_lens, cu_pre, pre_k, pre_v,
+                       case.kv_dtype, case.k_scale, case.v_scale)
+            if memo:
+                _PREFIX_POOLS[case.name] = (self.kp_ref.copy(), self.vp_ref.copy())
         if not prefix_on_gpu:
             self.cache = s2l.PagedKVCache(pool_to_dev(self.kp_ref), pool_to_dev(self.vp_ref),
                                           self.k_scale, self.v_scale)
@@ -109,12 +133,22 @@ class Setup:
         """(O, LSE, A, B): the oracle's output, log-sum-exp and the softmax-weighted means of
         |V| and of |V - O|.  q8: of the queries quantised per (token, head) row to e4m3."""
         c = self.case
+        # a named case's appended pools are the same in every test, so is the oracle's answer
+        key = None
+        if self.named and self.appended:
+            rows_key = None if sample_rows is None else tuple((r, tuple(v)) for r, v in sorted(sample_rows.items()))
+            key = (c.name, q8, rows_key)
+            if key in _ORACLE:
+                return _ORACLE[key]
         q = bf16_bits_to_f32(c.q_bits).astype(np.float64)
         if q8:
             q = quantize_rows(bf16_bits_to_f32(c.q_bits))[2]
-        return ref_batch_attn(q, self.kp_ref, self.vp_ref, self.tables, c.prefix_lens, c.chunk_lens,
-                              c.cu_chunk, c.num_q_heads, SCALE, c.kv_dtype, c.k_scale, c.v_scale,
-                              sample_rows=sample_rows, with_abs=True)
+        res = ref_batch_attn(q, self.kp_ref, self.vp_ref, self.tables, c.prefix_lens, c.chunk_lens,
+                             c.cu_chunk, c.num_q_heads, SCALE, c.kv_dtype, c.k_scale, c.v_scale,
+                             sample_rows=sample_rows, with_abs=True)
+        if key is not None:
+            _ORACLE[key] = res
+        return res
 
 
 def sample_rows(case, per_req, rng):

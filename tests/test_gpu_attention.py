@@ -7,7 +7,7 @@ import torch
 
 import paper_2604_16395_amd as s2l
 import workloads
-from tests.gpu_util import (DEV, SCALE, Setup, assert_attention_close, bf16_to_f64, from_bf16,
+from tests.gpu_util import (DEV, SCALE, Setup, named_case, assert_attention_close, bf16_to_f64, from_bf16,
                             sample_rows, to_bf16)
 
 pytestmark = pytest.mark.gpu
@@ -81,7 +81,7 @@ def test_peaky_and_growing_scores(q_sigma, k_ramp):
 
 @pytest.mark.parametrize("layout", LAYOUTS)
 def test_config2_sampled_rows(layout):
-    case = workloads.config2()
+    case = named_case("config2")
     s = Setup(case)
     s.append()
     out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1]))
@@ -102,7 +102,7 @@ def test_config4_mixed_batch_sampled_rows():
 
 @pytest.mark.parametrize("layout", [(128, 2), (256, 1)])
 def test_config5_fp8_cache_sampled_rows(layout):
-    case = workloads.config5()
+    case = named_case("config5")
     s = Setup(case)
     s.append()
     out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1]))

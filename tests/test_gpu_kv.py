@@ -7,7 +7,7 @@ import paper_2604_16395_amd as s2l
 import workloads
 from oracle.fp8_e4m3 import quantise_kv
 from oracle.paged_kv import bf16_bits_to_f32
-from tests.gpu_util import DEV, Setup, pool_from_dev, to_bf16
+from tests.gpu_util import DEV, Setup, named_case, pool_from_dev, to_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -39,7 +39,7 @@ def test_append_prefix_written_by_the_gpu_matches_too():
 
 
 def test_append_config2_and_fp8_config5_shapes():
-    _check_append(workloads.config2())
+    _check_append(named_case("config2"))
     c5 = workloads.make_case("p1000_c2048_h64kv8_fp8", [1000], [2048], 64, 8, seed=1005, kv_dtype="fp8",
                              pool_pages=200)
     _check_append(c5)

@@ -7,7 +7,7 @@ import torch
 
 import paper_2604_16395_amd as s2l
 import workloads
-from tests.gpu_util import DEV, SCALE, Setup, assert_attention_close, bf16_to_f64, sample_rows, to_bf16
+from tests.gpu_util import DEV, SCALE, Setup, named_case, assert_attention_close, bf16_to_f64, sample_rows, to_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -45,7 +45,7 @@ def test_q8_quantisation_is_applied():
 
 
 def test_q8_config5_sampled_rows():
-    case = workloads.config5()
+    case = named_case("config5")
     s = Setup(case)
     s.append()
     out, lse = s.attention(q8=True)
