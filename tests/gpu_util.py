@@ -68,7 +68,7 @@ class Setup:
     def __init__(self, case, block_tables=None, prefix_on_gpu=False):
         self.case = case
         self.tables = case.block_tables if block_tables is None else block_tables
-        self.named = block_tables is None and _NAMED.get(case.name) is case
+        self.named = block_tables is None and any(c is case for c in _NAMED.values())
         R = case.num_reqs
         zeros = np.zeros(R, np.int32)
         cu_pre = np.zeros(R + 1, np.int32)
