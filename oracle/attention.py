@@ -63,18 +63,21 @@ def ref_chunk_attn_loops(q, k, v, P, scale):
     return out, lse
 
 
-def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=None, with_abs=False):
+def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=None, with_abs=False,
+                           spread=True):
     """Blocked form of the same definition.
 
     q: [C][Hq][D]; k, v: [>= P+C][Hkv][D] (float64).  ``rows`` optionally selects query
     rows (sorted indices into the chunk); only those are computed and returned.
     Pass 1 finds each row's maximum score over all visible keys; pass 2 sums
     exp(s - m) and exp(s - m) V.  Blocks only bound memory: no term is reordered
-    beyond summation order.
+    beyond summation order.  Every contraction is a float64 matrix product (BLAS).
 
     ``with_abs`` also returns A = sum_j w_j |V_j| and B = sum_j w_j |V_j - O| (pass 3,
     once O is known), with w the softmax weights: per-element scales for rounding-error
-    bounds of an implementation that rounds the weights.
+    bounds of an implementation that rounds the weights.  With ``spread=False`` pass 3 is
+    skipped and B is returned as NaN (A alone costs one more matrix product; B needs
+    |V_j - O| for every key and row, which is not a matrix product).
     """
     C, hq, d = q.shape
     hkv = k.shape[1]
@@ -83,8 +86,17 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
     n_rows = len(rows)
     out = np.zeros((n_rows, hq, d))
     out_abs = np.zeros((n_rows, hq, d)) if with_abs else None
-    out_dev = np.zeros((n_rows, hq, d)) if with_abs else None
+    out_dev = np.full((n_rows, hq, d), np.nan) if with_abs else None
     lse = np.zeros((n_rows, hq))
+
+    def scores(qb, kb):                                  # [nb][G][D] x [j][D] -> [nb][G][j]
+        nb, gs, dd = qb.shape
+        return scale * (qb.reshape(nb * gs, dd) @ np.ascontiguousarray(kb).T).reshape(nb, gs, kb.shape[0])
+
+    def weighted(w, x):                                  # [nb][G][j] x [j][D] -> [nb][G][D]
+        nb, gs, j = w.shape
+        return (w.reshape(nb * gs, j) @ x).reshape(nb, gs, x.shape[1])
+
     for g in range(hkv):
         heads = slice(g * g_size, (g + 1) * g_size)
         for b0 in range(0, n_rows, q_block):
@@ -93,11 +105,18 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
             horizon = P + rb                             # last visible key per row
             kmax = int(horizon.max()) + 1
             m = np.full((len(rb), g_size), -np.inf)
+            def visible(k0, nk):                         # None: every key of the block is visible
+                if k0 + nk - 1 <= horizon.min():
+                    return None
+                keys = np.arange(k0, k0 + nk)
+                return keys[None, None, :] <= horizon[:, None, None]
+
             for k0 in range(0, kmax, k_block):           # pass 1: maxima
                 kb = k[k0:min(kmax, k0 + k_block), g, :]
-                s = scale * np.einsum("ngd,jd->ngj", qb, kb)
-                keys = np.arange(k0, k0 + kb.shape[0])
-                s = np.where(keys[None, None, :] <= horizon[:, None, None], s, -np.inf)
+                s = scores(qb, kb)
+                vis = visible(k0, kb.shape[0])
+                if vis is not None:
+                    s = np.where(vis, s, -np.inf)
                 m = np.maximum(m, s.max(axis=2))
             den = np.zeros((len(rb), g_size))
             acc = np.zeros((len(rb), g_size, d))
@@ -105,28 +124,32 @@ def ref_chunk_attn_blocked(q, k, v, P, scale, q_block=512, k_block=4096, rows=No
             for k0 in range(0, kmax, k_block):           # pass 2: sums
                 kb = k[k0:min(kmax, k0 + k_block), g, :]
                 vb = v[k0:min(kmax, k0 + k_block), g, :]
-                s = scale * np.einsum("ngd,jd->ngj", qb, kb)
-                keys = np.arange(k0, k0 + kb.shape[0])
-                w = np.where(keys[None, None, :] <= horizon[:, None, None],
-                             np.exp(s - m[:, :, None]), 0.0)
+                w = np.exp(scores(qb, kb) - m[:, :, None])
+                vis = visible(k0, kb.shape[0])
+                if vis is not None:
+                    w = np.where(vis, w, 0.0)
                 den += w.sum(axis=2)
-                acc += np.einsum("ngj,jd->ngd", w, vb)
+                acc += weighted(w, vb)
                 if with_abs:
-                    acc_abs += np.einsum("ngj,jd->ngd", w, np.abs(vb))
+                    acc_abs += weighted(w, np.abs(vb))
             o_blk = acc / den[:, :, None]
             out[b0:b0 + q_block, heads, :] = o_blk
             lse[b0:b0 + q_block, heads] = m + np.log(den)
             if with_abs:
                 out_abs[b0:b0 + q_block, heads, :] = acc_abs / den[:, :, None]
+            if with_abs and spread:
                 dev = np.zeros((len(rb), g_size, d))
-                for k0 in range(0, kmax, k_block):       # pass 3: spread about O
+                for k0 in range(0, kmax, k_block):       # pass 3: spread about O, row by row
                     kb = k[k0:min(kmax, k0 + k_block), g, :]
                     vb = v[k0:min(kmax, k0 + k_block), g, :]
-                    s = scale * np.einsum("ngd,jd->ngj", qb, kb)
-                    keys = np.arange(k0, k0 + kb.shape[0])
-                    w = np.where(keys[None, None, :] <= horizon[:, None, None],
-                                 np.exp(s - m[:, :, None]), 0.0)
-                    dev += np.einsum("ngj,ngjd->ngd", w, np.abs(vb[None, None, :, :] - o_blk[:, :, None, :]))
+                    w = np.exp(scores(qb, kb) - m[:, :, None])
+                    vis = visible(k0, kb.shape[0])
+                    if vis is not None:
+                        w = np.where(vis, w, 0.0)
+                    for i in range(len(rb)):
+                        for j0 in range(0, kb.shape[0], 512):   # [G][512][D] at a time
+                            spread_i = np.abs(vb[None, j0:j0 + 512, :] - o_blk[i][:, None, :])
+                            dev[i] += np.matmul(w[i][:, None, j0:j0 + 512], spread_i)[:, 0, :]
                 out_dev[b0:b0 + q_block, heads, :] = dev / den[:, :, None]
     if with_abs:
         return out, lse, out_abs, out_dev
@@ -196,14 +219,14 @@ def lse_merge(outs, lses):
 
 def ref_batch_attn(q_rows, k_pool, v_pool, block_tables, prefix_lens, chunk_lens, cu_chunk,
                    num_q_heads, scale, kv_dtype="bf16", k_scale=None, v_scale=None,
-                   sample_rows=None, method="blocked", with_abs=False):
+                   sample_rows=None, method="blocked", with_abs=False, spread=True):
     """Attention of a varlen batch whose K/V (prefix and chunk) are read through the pools.
 
     q_rows: float64 [T][Hq][D] (the chunk queries, request r at rows cu_chunk[r]..).
     Returns float64 O [T][Hq][D] and LSE [T][Hq] (rows not sampled are NaN when
     ``sample_rows`` is given as a dict r -> sorted chunk-row indices), and with
     ``with_abs`` the softmax-weighted means of |V| and of |V - O| [T][Hq][D] as a third and
-    a fourth array.
+    a fourth array (the fourth NaN with ``spread=False``, as in ``ref_chunk_attn_blocked``).
     """
     T = q_rows.shape[0]
     d = q_rows.shape[2]
@@ -227,7 +250,7 @@ def ref_batch_attn(q_rows, k_pool, v_pool, block_tables, prefix_lens, chunk_lens
             o, l = ref_chunk_attn_loops(q, k, v, P, scale)
             out[row0:row0 + C], lse[row0:row0 + C] = o, l
         else:
-            res = ref_chunk_attn_blocked(q, k, v, P, scale, rows=rows, with_abs=with_abs)
+            res = ref_chunk_attn_blocked(q, k, v, P, scale, rows=rows, with_abs=with_abs, spread=spread)
             idx = np.arange(C) if rows is None else np.asarray(rows)
             out[row0 + idx], lse[row0 + idx] = res[0], res[1]
             if with_abs:
