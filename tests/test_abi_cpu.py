@@ -35,7 +35,7 @@ def test_library_exports_every_declared_function():
 
 
 def test_abi_version():
-    assert _lib.lib().s2l_abi_version() == 2
+    assert _lib.lib().s2l_abi_version() == 3
 
 
 def _batch(P, C, max_pages=None, device=True):

@@ -7,8 +7,8 @@ import torch
 
 import paper_2604_16395_amd as s2l
 import workloads
-from tests.gpu_util import (DEV, SCALE, Setup, named_case, assert_attention_close, bf16_to_f64, from_bf16,
-                            sample_rows, to_bf16)
+from tests.gpu_util import (DEV, SCALE, Setup, named_case, assert_attention_close, bf16_to_f64, count_rows,
+                            dense_rows, from_bf16, sample_rows, to_bf16)
 
 pytestmark = pytest.mark.gpu
 
@@ -64,8 +64,11 @@ def test_config1_full_and_first_row_is_v0():
 
 @pytest.mark.parametrize("q_sigma,k_ramp", [(4.0, 0.0), (4.0, 3.0), (0.5, 6.0), (0.05, 0.0)])
 def test_peaky_and_growing_scores(q_sigma, k_ramp):
-    """Score spread of sigma ~2, keys that grow along the sequence (the running max rises
-    during the key loop and the rescaling path runs), and near-uniform scores."""
+    """Score spread of sigma ~2, keys that grow along the sequence (a later key's probability
+    reaches about 2^42 against the reference a key group starts from, per the host replay
+    gpu_util.rescale_excess: the common path's wide range), and near-uniform scores.  The
+    rescale branch itself (a probability above 2^64) is exercised by the planted keys of
+    test_gpu_rescale.py."""
     case = workloads.make_case("peaky", [3000, 100], [300, 64], 32, 8, seed=10, q_sigma=q_sigma,
                                k_ramp=k_ramp)
     ref = None
@@ -91,24 +94,32 @@ def test_config2_sampled_rows(layout):
 
 
 def test_config4_mixed_batch_sampled_rows():
+    """Every request: first and last chunk rows and 32 others (all rows of shorter chunks),
+    against the oracle with B bounded by A + |O|; 4 of them per request with the exact B."""
     case = workloads.config4()
     s = Setup(case)
     s.append()
     out, lse = s.attention()
-    rows = sample_rows(case, 4, np.random.default_rng(4))
-    ref = s.oracle(rows)
-    assert_attention_close(case, out, lse, ref, rows, what="cfg4")
+    rows = sample_rows(case, 32, np.random.default_rng(4))
+    assert all(len(v) >= min(32, int(case.chunk_lens[r])) for r, v in rows.items())
+    assert_attention_close(case, out, lse, s.oracle(rows, spread=False), rows, what="cfg4")
+    exact = sample_rows(case, 2, np.random.default_rng(44))
+    assert_attention_close(case, out, lse, s.oracle(exact), exact, what="cfg4 exact B")
 
 
 @pytest.mark.parametrize("layout", [(128, 2), (256, 1)])
 def test_config5_fp8_cache_sampled_rows(layout):
+    """Every 8th of the 2048 chunk rows and the last one (257 rows) against the oracle with B
+    bounded by A + |O|; 16 of them with the exact B."""
     case = named_case("config5")
     s = Setup(case)
     s.append()
     out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1]))
-    rows = sample_rows(case, 30, np.random.default_rng(5))
-    ref = s.oracle(rows)
-    assert_attention_close(case, out, lse, ref, rows, what="cfg5")
+    rows = dense_rows(case, 8)
+    assert count_rows(rows) >= 256
+    assert_attention_close(case, out, lse, s.oracle(rows, spread=False), rows, what="cfg5")
+    exact = dense_rows(case, 128)
+    assert_attention_close(case, out, lse, s.oracle(exact), exact, what="cfg5 exact B")
 
 
 def test_main_plus_reduce_equals_the_combined_call():
@@ -142,3 +153,23 @@ def test_small_fp8_cache_matches_oracle(split, layout):
     out, lse = s.attention(s2l.plan_opts(tile_cols=layout[0], key_halves=layout[1], **opts))
     ref = s.oracle()
     assert_attention_close(case, out, lse, ref, what="fp8_small")
+
+
+def test_device_lengths_beyond_the_host_plan_are_reported():
+    """The device length arrays are raised after the host copies were taken (the contract
+    forbids it; the condition is forced from the host and every kernel exits normally): the
+    device plan does not fit the host's sizing, so its status word is 1, and the attention
+    call writes NaN to every element of out and lse instead of leaving them stale.  Restored
+    lengths plan with status 0 and match the oracle."""
+    case = workloads.make_case("mismatch", [100, 200], [64, 32], 8, 2, seed=50)
+    s = Setup(case)
+    s.append()
+    opts = s2l.plan_opts(tile_cols=128)
+    s.batch.chunk_lens[1] = 200                      # device copy only: 7 query tiles, not 1
+    out, lse = s.attention(opts)
+    assert int(s2l.plan_status(s._ws).item()) == 1
+    assert torch.isnan(out.float()).all() and torch.isnan(lse).all()
+    s.batch.chunk_lens[1] = 32
+    out, lse = s.attention(opts)
+    assert int(s2l.plan_status(s._ws).item()) == 0
+    assert_attention_close(case, out, lse, s.oracle(), what="restored lengths")

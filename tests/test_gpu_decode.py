@@ -1,8 +1,8 @@
 """GPU: the decode kernel (16-column work items, chosen when every request has
 C * G <= 16) against the fp64 oracle: single tokens and a few tokens per tile (causal
 inside the tile), every G from 1 to 16, page-edge prefixes, split and unsplit key ranges
-(including pieces too short for all four waves), bf16 and fp8 caches, the overflow
-(rescale) path, and long prefixes."""
+(including pieces too short for all four waves), bf16 and fp8 caches, growing scores, and
+long prefixes."""
 import zlib
 
 import numpy as np
@@ -61,7 +61,9 @@ def test_decode_tiles_of_several_tokens_forced():
 @pytest.mark.parametrize("q_sigma,k_ramp", [(4.0, 3.0), (0.5, 6.0)])
 def test_decode_rescale_path(q_sigma, k_ramp):
     """Keys that grow along the sequence: a wave's reference max (its first tile) is
-    overtaken by far and the rescaling path runs."""
+    overtaken by far (probabilities up to about 2^30 against it, per the host replay
+    gpu_util.rescale_excess; the rescale branch, above 2^64, is exercised by the planted keys
+    of test_gpu_rescale.py)."""
     case = workloads.make_case("ramp", [6000, 300], [1, 1], 32, 8, seed=33, q_sigma=q_sigma, k_ramp=k_ramp)
     s = Setup(case)
     s.append()

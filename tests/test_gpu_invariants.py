@@ -6,7 +6,7 @@ import torch
 
 import paper_2604_16395_amd as s2l
 import workloads
-from tests.gpu_util import DEV, SCALE, Setup, assert_attention_close, bf16_to_f64, to_bf16
+from tests.gpu_util import DEV, SCALE, Setup, assert_attention_close, count_rows, dense_rows, to_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -68,8 +68,11 @@ def test_split_and_unsplit_agree_within_tolerance():
 
 def test_streaming_64_chunks_equals_one_shot_prefill():
     """Config 3: one 32768-token context arriving as 64 chunks of 512; each step appends its
-    K/V and attends over the growing prefix.  The concatenated outputs match the oracle's
-    one-shot causal prefill on sampled rows, and the GPU's own one-shot run everywhere."""
+    K/V and attends over the growing prefix.  The streamed outputs and the GPU's own one-shot
+    prefill (P = 0, C = 32768) both match the oracle's one-shot causal prefill on a dense,
+    deterministic row set: every 64th row and the first and last row of every chunk (576
+    rows), with B bounded by A + |O|; and on the last row of every 8th chunk with the exact
+    B."""
     case = workloads.config3_stream()
     kp = torch.full((case.num_pages, 8, 16, 128), 0, dtype=torch.int16, device=DEV)
     kp.fill_(0x7FBF)
@@ -88,24 +91,19 @@ def test_streaming_64_chunks_equals_one_shot_prefill():
         s2l.s2l_chunk_prefill_attn(cache, b, q_all[P:P + 512].contiguous(), 32, SCALE, out[P:P + 512], None,
                                    plan, ws)
     torch.cuda.synchronize()
-    # oracle on sampled rows of the whole sequence (P = 0, C = 32768 view of the same data)
     s = Setup(case)
-    rng = np.random.default_rng(3)
-    rows = {0: sorted(set(rng.integers(0, 32768, size=160).tolist()) | {0, 511, 512, 32767})}
     s.append()
-    ref = s.oracle(rows)
-    assert_attention_close(case, out, None, ref, rows, what="stream")
-    # GPU one-shot (P=0, C=32768): within the oracle bound on the sampled rows, and within
-    # twice that bound of the streamed run on every row.  With vmax = max |V| of the kv head,
-    # |O| <= vmax and B = sum_j w_j |V_j - O| <= 2 vmax, so each run is within
-    # u |O| + 4.04 u vmax (+ 2^-16 A + 1e-6) of the exact output, u = 2^-8.
     one, _ = s.attention()
+    assert torch.equal(kp, s.cache.k_pages.view(torch.int16)) and torch.equal(vp, s.cache.v_pages.view(torch.int16))
+    rows = dense_rows(case, 64, 512)
+    assert count_rows(rows) == 576
+    ref = s.oracle(rows, spread=False)
+    assert_attention_close(case, out, None, ref, rows, what="stream")
     assert_attention_close(case, one, None, ref, rows, what="one-shot")
-    a, b = bf16_to_f64(out), bf16_to_f64(one)
-    vmax = np.abs(bf16_to_f64(v_all)).max(axis=(0, 2))           # [Hkv]
-    vmax_q = np.repeat(vmax, 4)[None, :, None]                   # query head h reads kv head h // 4
-    u = 2.0 ** -8
-    assert (np.abs(a - b) <= 2 * u * 1.01 * np.abs(b) + 8.1 * u * vmax_q + 2 ** -15 * vmax_q + 2e-6).all()
+    exact = {0: [512 * c + 511 for c in range(0, 64, 8)]}
+    ref_b = s.oracle(exact)
+    assert_attention_close(case, out, None, ref_b, exact, what="stream exact B")
+    assert_attention_close(case, one, None, ref_b, exact, what="one-shot exact B")
 
 
 def test_back_to_back_launches_are_bit_identical():

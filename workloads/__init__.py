@@ -79,9 +79,43 @@ def _draw(rng, shape, sigma):
     return bf16_bits(rng.standard_normal(shape, dtype=np.float32) * np.float32(sigma))
 
 
+PLANT_OFFSET = 40   # planted keys sit at position 64 t + 40: never among the first 32 keys of a 64-key tile
+
+
+def _plant_keys(q_bits, kf, P, C, seq_lo, q_row, num_q_heads, num_kv_heads, dots, twin_gap):
+    """Keys aligned with one query (in place on the float32 keys ``kf`` of one request).
+
+    For each kv head g, the query of the chunk's last token at query head g*G (it sees every
+    key of the request) is the target: len(dots) keys at positions 64 t + PLANT_OFFSET, spread
+    evenly over the request's 64-key tiles from the second on, are replaced by
+    dots[i] * q / |q|^2, so that their dot product with the target query is dots[i] (before
+    bf16 rounding); the position after the last planted key gets dots[-1] - twin_gap.
+    Returns the planted positions."""
+    n = P + C
+    last_tile = (n - PLANT_OFFSET - 2) // 64          # 64 t + PLANT_OFFSET + 1 <= n - 1
+    if C <= 0 or last_tile < 1 or not dots:
+        return []
+    cnt = len(dots)
+    tiles = [1 + (t * (last_tile - 1)) // max(cnt - 1, 1) for t in range(cnt)]
+    by_tile = dict(zip(tiles, dots))                  # a request too short for all: the later win
+    pos = [64 * t + PLANT_OFFSET for t in sorted(by_tile)]
+    dots = [by_tile[t] for t in sorted(by_tile)]
+    G = num_q_heads // num_kv_heads
+    for g in range(num_kv_heads):
+        qb = q_bits[q_row + C - 1, g * G].astype(np.uint32) << 16
+        qv = qb.view(np.float32).astype(np.float64)
+        qq = float(qv @ qv)
+        if qq == 0.0:
+            continue
+        for j, dot in zip(pos, dots):
+            kf[seq_lo + j, g] = (dot / qq * qv).astype(np.float32)
+        kf[seq_lo + pos[-1] + 1, g] = ((dots[-1] - twin_gap) / qq * qv).astype(np.float32)
+    return pos
+
+
 def make_case(name, prefix_lens, chunk_lens, num_q_heads, num_kv_heads, seed,
               kv_dtype="bf16", pool_pages=None, table_mode="disjoint", sigma=0.5,
-              q_sigma=None, k_ramp=0.0, max_pages=None, rng=None):
+              q_sigma=None, k_ramp=0.0, max_pages=None, rng=None, plant_dots=None, plant_twin_gap=0.0):
     """Build one case from explicit lengths.
 
     table_mode: "disjoint" - request r takes a consecutive slice of one random
@@ -89,7 +123,10 @@ def make_case(name, prefix_lens, chunk_lens, num_q_heads, num_kv_heads, seed,
                 tests); "shared:<n>" - every request maps its first n pages to the same
                 physical pages (read-only shared prefix).
     k_ramp:     K row j of a request is multiplied by (1 + k_ramp * j / n) before bf16
-                rounding, so scores grow along the sequence (forces running-max updates).
+                rounding, so scores grow along the sequence.
+    plant_dots: keys aligned with one query per kv head (see ``_plant_keys``): a few keys
+                whose dot products with that query are these values, late in each request,
+                so that its scores rise far above those of the keys before them.
     """
     rng = np.random.default_rng(seed) if rng is None else rng
     P = np.asarray(prefix_lens, dtype=np.int32)
@@ -106,6 +143,7 @@ def make_case(name, prefix_lens, chunk_lens, num_q_heads, num_kv_heads, seed,
     q_bits = np.empty((int(cu_chunk[-1]), num_q_heads, d), dtype=np.uint16)
     k_bits = np.empty((int(cu_seq[-1]), num_kv_heads, d), dtype=np.uint16)
     v_bits = np.empty_like(k_bits)
+    planted = {}
     for r in range(R):
         q_bits[cu_chunk[r]:cu_chunk[r + 1]] = _draw(rng, (int(C[r]), num_q_heads, d), q_sigma)
     for r in range(R):
@@ -113,6 +151,9 @@ def make_case(name, prefix_lens, chunk_lens, num_q_heads, num_kv_heads, seed,
         kf = rng.standard_normal((n, num_kv_heads, d), dtype=np.float32) * np.float32(sigma)
         if k_ramp:
             kf *= (1.0 + k_ramp * np.arange(n, dtype=np.float32) / max(n, 1))[:, None, None]
+        if plant_dots:
+            planted[r] = _plant_keys(q_bits, kf, int(P[r]), int(C[r]), 0, int(cu_chunk[r]), num_q_heads,
+                                     num_kv_heads, list(plant_dots), plant_twin_gap)
         k_bits[cu_seq[r]:cu_seq[r + 1]] = bf16_bits(kf)
         del kf
     for r in range(R):
@@ -157,7 +198,8 @@ def make_case(name, prefix_lens, chunk_lens, num_q_heads, num_kv_heads, seed,
         vf = (v_bits.astype(np.uint32) << 16).view(np.float32)
         case.k_scale = (np.abs(kf).max(axis=(0, 2)) / np.float32(448.0)).astype(np.float32)
         case.v_scale = (np.abs(vf).max(axis=(0, 2)) / np.float32(448.0)).astype(np.float32)
-    case.meta = dict(seed=seed, sigma=sigma, q_sigma=q_sigma, k_ramp=k_ramp, table_mode=table_mode)
+    case.meta = dict(seed=seed, sigma=sigma, q_sigma=q_sigma, k_ramp=k_ramp, table_mode=table_mode,
+                     planted=planted)
     return case
 
 
