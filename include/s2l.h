@@ -30,9 +30,10 @@
  *     A failed launch returns S2L_EHIP.  Device faults surface at the caller's next sync.
  *   - Preconditions that are not checked (undefined behaviour if violated): block-table
  *     entries for the pages a request uses lie in [0, num_pages); device length arrays hold
- *     the same values as their host copies; pages written by an append belong to that
- *     request alone (shared prefix pages are read-only); no two in-flight calls share a
- *     workspace.
+ *     the same values as their host copies (a difference that needs more work than the
+ *     host planned for is reported by the plan's status word, see s2l_attn_plan); pages
+ *     written by an append belong to that request alone (shared prefix pages are
+ *     read-only); no two in-flight calls share a workspace.
  */
 #ifndef S2L_H
 #define S2L_H
@@ -44,9 +45,12 @@
 extern "C" {
 #endif
 
-#define S2L_ABI_VERSION 2
+#define S2L_ABI_VERSION 3
 #define S2L_HEAD_DIM 128
 #define S2L_PAGE_SIZE 16
+/* Byte offset, in a workspace that s2l_attn_plan has filled, of the plan's int32 status word
+ * (see s2l_attn_plan). */
+#define S2L_PLAN_STATUS_OFFSET 36
 
 typedef enum s2l_status {
   S2L_OK = 0,
@@ -159,11 +163,18 @@ s2l_status s2l_kv_append(const s2l_kv_cache* cache, const s2l_batch* batch,
                          const void* k_new, const void* v_new, void* stream);
 
 /*
- * Copy stored K/V elements of positions 0..n_r-1 of every request out of the pages,
- * bit-exact (bf16 bits or fp8 codes, not dequantised); n_r = P_r + C_r if include_chunk,
- * else P_r.  Request r's rows go to rows cu_out[r] .. cu_out[r] + n_r - 1 of k_out / v_out,
- * each [rows][Hkv][128] elements of the cache dtype.  For testing and for swap-out.
+ * Read a request's cached K/V back out of its pages in position order: the inverse of the
+ * block-table addressing of Sec. 2.2 (block j of a request holds tokens (j-1)k+1 .. jk,
+ * anywhere in the pool), as a preempted request's blocks are copied out when it is swapped
+ * to CPU memory (Sec. 2.2 swapping; Sec. 4.3 cost-based preemption).  Copies stored K/V
+ * elements of positions 0..n_r-1 of every request, bit-exact (bf16 bits or fp8 codes, not
+ * dequantised); n_r = P_r + C_r if include_chunk, else P_r.  Request r's rows go to rows
+ * cu_out[r] .. cu_out[r] + n_r - 1 of k_out / v_out, each [rows][Hkv][128] elements of the
+ * cache dtype.  Used by the tests and as the dense form of a swap-out.
  *   cu_out : device int32 [R+1] row offsets chosen by the caller (need not be dense).
+ *   k_out, v_out: device, caller-owned, at least max_r(cu_out[r] + n_r) rows.
+ * Errors: EINVAL (nulls, negative lengths), ERANGE (P_r + C_r > max_pages_per_req * 16),
+ * ENOTSUP (head_dim/page_size), EHIP.
  */
 s2l_status s2l_kv_gather(const s2l_kv_cache* cache, const s2l_batch* batch, int32_t include_chunk,
                          const int32_t* cu_out, void* k_out, void* v_out, void* stream);
@@ -199,16 +210,25 @@ s2l_status s2l_kv_swap_in(const s2l_kv_cache* cache, const int32_t* pairs, int32
                           const void* host_v, int32_t num_host_pages, void* stream);
 
 /*
- * Workspace bytes that s2l_attn_plan and the attention calls need for this batch (host
- * computation from the host length copies; opts as for s2l_attn_plan).
+ * Workspace bytes that s2l_attn_plan and the attention calls need for one scheduler step's
+ * batch (Sec. 4.1: each step runs the continuous batch of selected requests, their new
+ * tokens limited by the token budget; Sec. 6.1 runs 2048-8192 tokens per step): the plan
+ * header, per-request arrays, one 64-byte record per work item and the fp32 partials of
+ * split key ranges.  A host computation from the host length copies (opts as for
+ * s2l_attn_plan); nothing is enqueued.
+ *   bytes_out: HOST out.
+ * Errors: EINVAL (nulls, negative lengths, bad head counts, negative opts), ENOTSUP
+ * (tile_cols / key_halves), EHIP (the CU count query, when target_items is 0).
  */
 s2l_status s2l_attn_workspace_bytes(const s2l_batch* batch, int32_t num_q_heads, int32_t num_kv_heads,
                                     const s2l_plan_opts* opts, size_t* bytes_out);
 
 /*
- * Build the varlen work partition for one step and store it in the workspace (a small
- * kernel on `stream`: per-request arrays and one 64-byte record per work item); reuse it
- * for every layer of the step.  Each request's chunk is cut into query tiles of
+ * Build the varlen work partition for one scheduler step (Sec. 4.1: a continuous batch of
+ * requests, each with num_computed_tokens cached and a share of the step's token budget as
+ * new tokens; Sec. 2.2 continuous batching) and store it in the workspace (a small kernel on
+ * `stream`: per-request arrays and one 64-byte record per work item); reuse it for every
+ * layer of the step.  Each request's chunk is cut into query tiles of
  * tile_cols / G tokens x G heads per kv head.  When the batch has fewer than target_items
  * tiles, each request's key range 0 .. P_r + i_end is split into up to max_splits pieces of
  * >= min_split_keys keys (never more items than target_items in total), so that long
@@ -217,6 +237,15 @@ s2l_status s2l_attn_workspace_bytes(const s2l_batch* batch, int32_t num_q_heads,
  * further halved between two wave groups of its workgroup, merged in LDS.
  *   workspace : device, ws_bytes >= s2l_attn_workspace_bytes(...).
  *   info      : HOST out, describes the plan; pass it to the attention calls.
+ * The device kernel plans from the device length arrays, sized by the host copies.  Its
+ * int32 status word (workspace byte S2L_PLAN_STATUS_OFFSET, readable once the stream has
+ * passed the plan) is 0 when the plan was stored, 1 when the device lengths need more work
+ * items, tiles or partial space than the host copies planned for (the two disagree, which
+ * the contract forbids): then nothing is planned, and every attention call on this plan
+ * computes nothing and writes NaN to every element of out (and lse).  Device lengths that
+ * differ from the host copies but fit are not detected.
+ * Errors: as s2l_attn_workspace_bytes, plus EINVAL (device arrays NULL), ERANGE, EWORKSPACE
+ * (workspace NULL or too small), EHIP (launch).
  */
 s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t num_kv_heads,
                          const s2l_plan_opts* opts, void* workspace, size_t ws_bytes,

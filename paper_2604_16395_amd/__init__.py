@@ -26,7 +26,7 @@ __all__ = ["PagedKVCache", "Batch", "plan_opts", "S2LError", "S2LLibraryMissing"
            "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in",
            "s2l_check_tables", "s2l_append_chunk_prefill_attn", "s2l_calib_stream_read", "s2l_calib_mfma_bf16", "s2l_attn_workspace_bytes",
            "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_chunk_prefill_attn_q8", "s2l_attn_main", "s2l_split_reduce",
-           "s2l_plan_host", "library_path"]
+           "s2l_plan_host", "library_path", "plan_status"]
 
 HEAD_DIM = 128
 PAGE_SIZE = 16
@@ -208,6 +208,18 @@ def s2l_attn_plan(batch, num_q_heads, num_kv_heads, workspace, opts=None, stream
     _lib.call("s2l_attn_plan", ctypes.byref(bc), num_q_heads, num_kv_heads, _opts_ptr(opts),
               _ptr(workspace), workspace.numel(), ctypes.byref(info), _stream(stream))
     return info
+
+
+PLAN_STATUS_OFFSET = 36      # S2L_PLAN_STATUS_OFFSET of include/s2l.h
+
+
+def plan_status(workspace):
+    """The plan's int32 status word in `workspace` (a device uint8 tensor that s2l_attn_plan
+    filled), as a 0-dim device tensor: 0 = planned, 1 = the device length arrays needed more
+    than the host copies planned for (the attention calls then write NaN and compute
+    nothing).  Read it after the stream has passed the plan."""
+    _check(workspace, torch.uint8, "workspace")
+    return workspace[PLAN_STATUS_OFFSET:PLAN_STATUS_OFFSET + 4].view(torch.int32)[0]
 
 
 def _attn(name, cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, stream):

@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <cstddef>
 #include <cstdarg>
 #include <cstdio>
 #include <string>
@@ -18,6 +19,9 @@
 namespace {
 thread_local std::string g_err;
 }  // namespace
+
+static_assert(offsetof(s2l::PlanHeader, status) == S2L_PLAN_STATUS_OFFSET,
+              "the plan status word sits where the header says");
 
 namespace s2l {
 
@@ -328,6 +332,7 @@ s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const 
   a.knew = k_new;
   a.vnew = v_new;
   a.q8 = q8;
+  a.total_rows = T;
   (void)hipGetLastError();
   hipError_t e = s2l::launch_attn_main(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail("attn_main launch", e);

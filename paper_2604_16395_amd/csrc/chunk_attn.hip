@@ -168,7 +168,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     void* kpool, void* vpool, const float* __restrict__ kscale,
     const float* __restrict__ vscale, const int32_t* __restrict__ block_tables, int32_t max_pages, int32_t hq,
     int32_t hkv, float scale_log2, PlanPtrs pv, int32_t group_by_xcd, const uint16_t* __restrict__ knew,
-    const uint16_t* __restrict__ vnew) {
+    const uint16_t* __restrict__ vnew, int64_t total_rows) {
   using RingT = Ring<kFp8, kColWaves, kHalves>;
   constexpr int kWaves = kColWaves * kHalves;
   constexpr int kS = RingT::kStages;
@@ -191,7 +191,11 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
   const int w_item = group_by_xcd ? xcd_logical(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const ItemRec it = pv.items[w_item];
   const int W = pv.hdr->num_items;
-  if (w_item >= W) return;   // the device plan did not fit this launch (nothing planned)
+  if (pv.hdr->status != 0) {   // the device plan did not fit this launch: nothing planned
+    poison_outputs(out, lse, total_rows, hq);
+    return;
+  }
+  if (w_item >= W) return;
   const int P = it.p, C = it.c, row0 = it.row0, ns = it.ns, g = it.g;
   const int i0 = it.i0, i1 = it.i1;
   const int G = hq / hkv;
@@ -943,7 +947,7 @@ void launch_main_variant(const AttnLaunch& a, hipStream_t stream) {
       static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
       a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, a.softmax_scale * kLog2e,
       plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0, static_cast<const uint16_t*>(a.knew),
-      static_cast<const uint16_t*>(a.vnew));
+      static_cast<const uint16_t*>(a.vnew), a.total_rows);
 }
 
 template <bool kFp8>

@@ -80,12 +80,16 @@ __global__ __launch_bounds__(kDecodeWaves * 64, 1) void attn_decode_kernel(
     const uint16_t* __restrict__ q, uint16_t* __restrict__ out, float* __restrict__ lse,
     const void* __restrict__ kpool, const void* __restrict__ vpool, const float* __restrict__ kscale,
     const float* __restrict__ vscale, const int32_t* __restrict__ block_tables, int32_t max_pages, int32_t hq,
-    int32_t hkv, float scale_log2, PlanPtrs pv, int32_t group_by_xcd) {
+    int32_t hkv, float scale_log2, PlanPtrs pv, int32_t group_by_xcd, int64_t total_rows) {
   __shared__ __attribute__((aligned(1024))) uint8_t smem[kDecodeWaves * kVWaveBytes];
 
   const int w_item = group_by_xcd ? xcd_logical(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const ItemRec it = pv.items[w_item];
-  if (w_item >= pv.hdr->num_items) return;   // the device plan did not fit this launch
+  if (pv.hdr->status != 0) {   // the device plan did not fit this launch: nothing planned
+    poison_outputs(out, lse, total_rows, hq);
+    return;
+  }
+  if (w_item >= pv.hdr->num_items) return;
   const int P = it.p, C = it.c, row0 = it.row0, ns = it.ns, g = it.g;
   const int i0 = it.i0, i1 = it.i1, lo = it.lo, hi = it.hi;
   const int G = hq / hkv;
@@ -369,12 +373,12 @@ hipError_t launch_attn_decode(const AttnLaunch& a, hipStream_t stream) {
     attn_decode_kernel<true><<<(unsigned)a.dims.num_items, kDecodeWaves * 64, 0, stream>>>(
         static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
         a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, scale_log2,
-        plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0);
+        plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0, a.total_rows);
   } else {
     attn_decode_kernel<false><<<(unsigned)a.dims.num_items, kDecodeWaves * 64, 0, stream>>>(
         static_cast<const uint16_t*>(a.q), static_cast<uint16_t*>(a.out), a.lse, a.kv.kpool, a.kv.vpool,
         a.kv.kscale, a.kv.vscale, a.kv.block_tables, a.kv.max_pages, a.hq, a.kv.hkv, scale_log2,
-        plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0);
+        plan_ptrs(a.workspace, a.dims), a.group_by_xcd ? 1 : 0, a.total_rows);
   }
   return hipGetLastError();
 }

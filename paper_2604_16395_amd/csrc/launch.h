@@ -74,6 +74,8 @@ struct AttnLaunch {
   const void* knew = nullptr;   // fused append (bf16, page-aligned prefixes): the chunk's
   const void* vnew = nullptr;   //   new K/V rows [T][Hkv][128], else null
   bool q8 = false;              // e4m3 pages: Q quantised per column, S on the fp8 MFMA
+  int64_t total_rows = 0;       // T of the host lengths: rows of out / lse (written as NaN
+                                //   when the device plan's status says it did not fit)
 };
 hipError_t launch_attn_main(const AttnLaunch& a, hipStream_t stream);
 

@@ -75,4 +75,20 @@ __device__ inline float sum_with_partner(float x) {
   return x;
 }
 
+// Outputs of a launch whose device plan did not fit the host's sizing (its status word is
+// not 0: the device length arrays disagree with the host copies, and nothing was planned).
+// Every workgroup writes NaN over its share of the `rows` output rows the host sized the
+// call for (rows blockIdx.x, blockIdx.x + gridDim.x, ...: out [rows][hq][128] bf16, lse
+// [rows][hq] fp32), so that the failure shows in the results instead of stale memory.
+__device__ inline void poison_outputs(uint16_t* out, float* lse, int64_t rows, int32_t hq) {
+  const int64_t chunks = (int64_t)hq * 16;            // 16-byte chunks of one output row
+  for (int64_t r = blockIdx.x; r < rows; r += gridDim.x) {
+    uint16_t* orow = out + r * hq * 128;
+    for (int64_t c = threadIdx.x; c < chunks; c += blockDim.x)
+      *reinterpret_cast<u32x4*>(orow + 8 * c) = u32x4{0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u, 0x7FC07FC0u};
+    if (lse != nullptr)
+      for (int h = threadIdx.x; h < hq; h += blockDim.x) lse[r * hq + h] = __builtin_nanf("");
+  }
+}
+
 }  // namespace s2l
