@@ -155,13 +155,14 @@ class Setup:
 
 
 def sample_rows(case, per_req, rng):
-    """Chunk rows to check per request: first, last, and `per_req` random others."""
+    """Chunk rows to check per request: first, last, and `per_req` distinct random others (every
+    row of a chunk shorter than that)."""
     out = {}
     for r in range(case.num_reqs):
         C = int(case.chunk_lens[r])
         if C == 0:
             continue
-        pick = {0, C - 1} | set(rng.integers(0, C, size=min(per_req, C)).tolist())
+        pick = {0, C - 1} | set(rng.choice(C, size=min(per_req, C), replace=False).tolist())
         out[r] = sorted(pick)
     return out
 
