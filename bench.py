@@ -60,76 +60,135 @@ def traffic_from_profile(src_hash):
     return float(m_bytes.group(1))
 
 
-def cpu_baseline(case, min_seconds=10.0, max_reps=5):
-    """The fp64 oracle on the whole workload (all 512 rows x 32 heads), repeated until at
-    least `min_seconds` have elapsed."""
-    from oracle.attention import ref_batch_attn
-    from oracle.paged_kv import bf16_bits_to_f32, ref_append
-    import workloads
-    R = case.num_reqs
-    shape = (case.num_pages, case.num_kv_heads, 16, 128)
-    kp = np.full(shape, workloads.BF16_SENTINEL, np.uint16)
-    vp = np.full(shape, workloads.BF16_SENTINEL, np.uint16)
-    seq = (case.prefix_lens + case.chunk_lens).astype(np.int32)
-    cu = np.zeros(R + 1, np.int32)
-    cu[1:] = np.cumsum(seq)
-    ref_append(kp, vp, case.block_tables, np.zeros(R, np.int32), seq, cu, case.k_full_bits, case.v_full_bits)
-    q = bf16_bits_to_f32(case.q_bits).astype(np.float64)
-    threads = None
+def cpu_model():
+    """The host CPU's model name (from /proc/cpuinfo) and its logical CPU count."""
+    name = "unknown"
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count()
-    reps, t0 = 0, time.perf_counter()
-    while True:
-        ref_batch_attn(q, kp, vp, case.block_tables, case.prefix_lens, case.chunk_lens, case.cu_chunk,
-                       case.num_q_heads, 1.0 / np.sqrt(128.0))
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= min_seconds or reps >= max_reps:
-            break
-    import workloads as wl
-    flops = wl.attn_flops(case.prefix_lens, case.chunk_lens, case.num_q_heads) * reps
-    res = {"value": flops / el / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-           "sample": f"whole workload (512 rows x 32 heads, fp64 numpy, blocked two-pass), {reps} rep(s), "
-                     f"{el:.1f} s"}
-    # the same oracle on one core, over every 8th chunk row (its keys are the same prefix plus
-    # the causal part up to the row): FLOPs of exactly those rows
-    try:
-        from threadpoolctl import threadpool_limits
-        rows = {0: list(range(0, int(case.chunk_lens[0]), 8))}
-        P0 = int(case.prefix_lens[0])
-        f1 = 4.0 * 128 * case.num_q_heads * sum(P0 + i + 1 for i in rows[0])
-        with threadpool_limits(1):
-            t1 = time.perf_counter()
-            ref_batch_attn(q, kp, vp, case.block_tables, case.prefix_lens, case.chunk_lens, case.cu_chunk,
-                           case.num_q_heads, 1.0 / np.sqrt(128.0), sample_rows=rows)
-            e1 = time.perf_counter() - t1
-        res["one_core"] = {"value": f1 / e1 / 1e12, "unit": "TFLOP/s", "cores": 1,
-                           "sample": f"every 8th chunk row ({len(rows[0])} rows x 32 heads), {e1:.1f} s"}
-    except ImportError:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
         pass
-    # the small configuration (one request, P=256, C=128, 8q/2kv) with both oracle forms: the
-    # per-row loops and the blocked form
+    return {"model": name, "logical_cpus": os.cpu_count()}
+
+
+def _oracle_samples(threads):
+    """The fp64 oracle on a bounded sample of every named workload, with its BLAS limited to
+    `threads` threads (set through the environment of this process before numpy loads).
+    Each sample: the workload's request shapes and head counts, seeded N(0, 0.5^2) inputs
+    (bf16-rounded where they go through the pools), the oracle's blocked attention on a subset
+    of chunk rows (each row over all of its visible keys), and the exact algorithmic FLOPs of
+    those rows (4 d Hq per visible key)."""
+    import workloads
+    from oracle.attention import ref_batch_attn, ref_chunk_attn_blocked
+    from oracle.paged_kv import bf16_bits_to_f32, ref_append
+    one = threads == 1
+    out = {}
+    scale = 1.0 / np.sqrt(128.0)
+
+    def flops_of(P, rows, hq):
+        return 4.0 * 128 * hq * sum(P + i + 1 for i in rows)
+
+    def dense(rng, n, h):              # N(0, 0.5^2) float64 (the values do not change the work)
+        x = rng.standard_normal((n, h, 128))
+        x *= 0.5
+        return x
+
+    # one K/V draw, as long as the longest request of any workload (8 kv heads everywhere),
+    # serves every request below (its first P + C rows); only sampled query rows are drawn
+    rng_kv = np.random.default_rng(7)
+    k_all, v_all = dense(rng_kv, 131072 + 2048, 8), dense(rng_kv, 131072 + 2048, 8)
+
+    def run_dense(name, reqs, hq, hkv, every, what):
+        """reqs: [(P, C)]; rows 0, every, 2 every, ... and C - 1 of each request."""
+        rng = np.random.default_rng(8)
+        k, v = k_all[:, :hkv], v_all[:, :hkv]
+        f, el = 0.0, 0.0
+        nrows = 0
+        for P, C in reqs:
+            rows = sorted(set(range(0, C, every)) | {C - 1})
+            q = np.zeros((C, hq, 128))
+            q[rows] = dense(rng, len(rows), hq)
+            t = time.perf_counter()
+            ref_chunk_attn_blocked(q, k[:P + C], v[:P + C], P, scale, rows=rows)
+            el += time.perf_counter() - t
+            f += flops_of(P, rows, hq)
+            nrows += len(rows)
+        out[name] = {"value": f / el / 1e12, "seconds": round(el, 2),
+                     "sample": f"{what}: {nrows} chunk rows x {hq} heads, each over all its visible keys"}
+
+    # config 1 (P=256, C=128, 8q/2kv), whole, through the pools: the loop and blocked forms
     c1 = workloads.config1()
     shape1 = (c1.num_pages, c1.num_kv_heads, 16, 128)
     kp1 = np.full(shape1, workloads.BF16_SENTINEL, np.uint16)
     vp1 = np.full(shape1, workloads.BF16_SENTINEL, np.uint16)
     seq1 = (c1.prefix_lens + c1.chunk_lens).astype(np.int32)
-    cu1 = np.zeros(c1.num_reqs + 1, np.int32)
+    cu1 = np.zeros(2, np.int32)
     cu1[1:] = np.cumsum(seq1)
-    ref_append(kp1, vp1, c1.block_tables, np.zeros(c1.num_reqs, np.int32), seq1, cu1, c1.k_full_bits, c1.v_full_bits)
+    ref_append(kp1, vp1, c1.block_tables, np.zeros(1, np.int32), seq1, cu1, c1.k_full_bits, c1.v_full_bits)
     q1 = bf16_bits_to_f32(c1.q_bits).astype(np.float64)
-    f1 = wl.attn_flops(c1.prefix_lens, c1.chunk_lens, c1.num_q_heads)
-    res["config1"] = {"unit": "TFLOP/s"}
+    f1 = workloads.attn_flops(c1.prefix_lens, c1.chunk_lens, c1.num_q_heads)
+    out["config1"] = {"sample": "whole config 1 through the pools, once per oracle form"}
     for method in ("loops", "blocked"):
-        t1 = time.perf_counter()
+        t = time.perf_counter()
         ref_batch_attn(q1, kp1, vp1, c1.block_tables, c1.prefix_lens, c1.chunk_lens, c1.cu_chunk,
-                       c1.num_q_heads, 1.0 / np.sqrt(128.0), method=method)
-        e1 = time.perf_counter() - t1
-        res["config1"][method] = {"value": f1 / e1 / 1e12, "seconds": round(e1, 3)}
-    res["config1"]["sample"] = "whole config 1 (P=256, C=128, 8q/2kv), once per oracle form"
+                       c1.num_q_heads, scale, method=method)
+        e = time.perf_counter() - t
+        out["config1"][method] = {"value": f1 / e / 1e12, "seconds": round(e, 3)}
+    # the headline step (config 3 at P = 8192), whole, through the pools
+    case = workloads.config3_step(16)
+    R = 1
+    kp = np.full((case.num_pages, 8, 16, 128), workloads.BF16_SENTINEL, np.uint16)
+    vp = kp.copy()
+    seq = (case.prefix_lens + case.chunk_lens).astype(np.int32)
+    ref_append(kp, vp, case.block_tables, np.zeros(R, np.int32), seq, np.array([0, seq[0]], np.int32),
+               case.k_full_bits, case.v_full_bits)
+    q = bf16_bits_to_f32(case.q_bits).astype(np.float64)
+    rows = {0: list(range(0, 512, 8 if one else 2))}
+    t = time.perf_counter()
+    ref_batch_attn(q, kp, vp, case.block_tables, case.prefix_lens, case.chunk_lens, case.cu_chunk, 32, scale,
+                   sample_rows=rows)
+    e = time.perf_counter() - t
+    out["headline"] = {"value": flops_of(8192, rows[0], 32) / e / 1e12, "seconds": round(e, 2),
+                       "sample": f"P=8192, C=512, 32q/8kv through the pools: {len(rows[0])} of 512 chunk rows"}
+    k = 4 if one else 1
+    P2, C2, _ = workloads.config2_lengths()
+    run_dense("config2", list(zip(P2.tolist(), C2.tolist())), 32, 8, 8 * k,
+              "config 2 (8 requests, P ~ U{0..8192}, C = 512, 32q/8kv)")
+    run_dense("config3", [(0, 32768)], 32, 8, 128 * k, "config 3 as its one-shot equivalent (32768 causal tokens)")
+    P4, C4, _ = workloads.config4_lengths()
+    reqs4 = list(zip(P4.tolist(), C4.tolist()))
+    run_dense("config4", reqs4[::4] if one else reqs4, 32, 8, 1 << 20,
+              "config 4 (64 requests, P ~ U{0..32768}, log-normal C): the first and last row of "
+              + ("every 4th request" if one else "every request"))
+    run_dense("config5", [(131072, 2048)], 64, 8, 256 * (3 if one else 1),
+              "config 5 (P = 131072, C = 2048, 64q/8kv; K/V as the decoded e4m3 cache's fp64 values)")
+    return out
+
+
+def cpu_baseline():
+    """The fp64 oracle timed on this machine's host cores: every named workload on a bounded
+    sample, once with the BLAS on all the cores this job has and once on one core, each in a
+    child process whose BLAS thread count is fixed before numpy loads."""
+    import subprocess
+    cores = int(os.environ.get("OMP_NUM_THREADS") or os.cpu_count() or 1)
+    runs = {}
+    for threads in (cores, 1):
+        env = dict(os.environ, OMP_NUM_THREADS=str(threads), OPENBLAS_NUM_THREADS=str(threads),
+                   MKL_NUM_THREADS=str(threads), BLIS_NUM_THREADS=str(threads))
+        p = subprocess.run([sys.executable, os.path.abspath(__file__), "--oracle-samples"], env=env,
+                           capture_output=True, text=True, timeout=900)
+        if p.returncode != 0:
+            raise RuntimeError(f"oracle sample run failed: {p.stderr[-2000:]}")
+        runs[threads] = json.loads(p.stdout.strip().splitlines()[-1])
+    head = runs[cores]["headline"]
+    res = {"value": round(head["value"], 5), "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+           "sample": head["sample"] + f" ({head['seconds']} s), fp64 numpy",
+           "cpu": cpu_model(),
+           "all_cores": {k: v for k, v in runs[cores].items() if k != "headline"},
+           "one_core": runs[1]}
     return res
 
 
@@ -159,7 +218,13 @@ def main():
                          "that clocks and power reach the steady state of sustained load")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain 1 GiB device copy (for counter calibration) and exit")
+    ap.add_argument("--oracle-samples", action="store_true",
+                    help="(internal) time the CPU oracle on samples of every workload and print JSON; "
+                         "no GPU is used")
     args = ap.parse_args()
+    if args.oracle_samples:
+        print(json.dumps(_oracle_samples(int(os.environ.get("OPENBLAS_NUM_THREADS", "0")))), flush=True)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (single-GPU build)",
               file=sys.stderr)
@@ -347,6 +412,8 @@ def main():
     assert torch.isfinite(out.float()).all(), "non-finite attention output"
 
     flops = workloads.attn_flops([P], [C], HQ)             # one layer
+    # algorithmic HBM bytes of one attention launch: K and V of every visible key, Q in, O out
+    algo_bytes = float((P + C) * HKV * 128 * 2 * 2 + 2 * C * HQ * 128 * 2)
     ms_per_layer = ms_per_step / L
     value = flops / (ms_per_layer * 1e-3) / 1e12
     achieved = flops / (main_ms * 1e-3) / 1e12
@@ -389,7 +456,9 @@ def main():
                    "why": "clocks reach the steady state of sustained load before timing"},
         "roofline": {"bound": "mfma", "kernel": "attn_main_kernel", "achieved": round(achieved, 2),
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
-                     "traffic": traffic, "kernel_source_sha256_16": src_hash},
+                     "traffic": traffic, "algorithmic_bytes": algo_bytes,
+                     "traffic_ratio": None if traffic is None else round(traffic / algo_bytes, 3),
+                     "us_per_launch": round(main_ms * 1e3, 2), "kernel_source_sha256_16": src_hash},
     }
     if fused_ms is not None:
         result["fused_append_step"] = {
@@ -414,7 +483,7 @@ def main():
         from paper_2604_16395_amd.benchcfg import all_configs
         result["other_configs"] = all_configs()
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(case)
+        result["cpu_baseline"] = cpu_baseline()
     print(json.dumps(result), flush=True)
 
 
