@@ -307,6 +307,29 @@ s2l_status s2l_chunk_prefill_attn_q8(const s2l_kv_cache* cache, const s2l_batch*
                                      const s2l_plan_info* plan, void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * s2l_chunk_prefill_attn for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same plan and the same
+ * attention and merge launches, with the workspace replaced by a scratch array the library
+ * holds on each GPU (S2L_NOALLOC_SCRATCH_BYTES, a file-scope device array that every GPU the
+ * library runs on keeps until the process ends).  Plans the batch (opts as for s2l_attn_plan,
+ * NULL for the defaults) and runs attention; results are bit-identical to s2l_attn_plan +
+ * s2l_chunk_prefill_attn with a caller workspace and the same opts.  The caller still passes
+ * q, out and lse; *plan_out (may be NULL) receives the plan's description.
+ * Allocates nothing: no hipMalloc, hipFree or allocating library routine.  The scratch holds
+ * the last call's plan and partials; every call writes all of it that it reads, so nothing
+ * needs clearing.  All calls on one GPU share its scratch: calls that overlap in time on one
+ * GPU (different streams or threads without ordering between them) race and give undefined
+ * results.
+ * Errors: as s2l_chunk_prefill_attn, plus EWORKSPACE when the batch needs more workspace than
+ * the scratch holds (s2l_attn_workspace_bytes tells), EHIP when the scratch's device address
+ * cannot be taken.
+ */
+#define S2L_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+s2l_status s2l_chunk_prefill_attn_noalloc(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q,
+                                          int32_t num_q_heads, float softmax_scale, void* out, float* lse,
+                                          const s2l_plan_opts* opts, s2l_plan_info* plan_out, void* stream);
+
+/*
  * The main attention kernel alone (online softmax over the work items of the plan).
  * Unsplit requests get their final out/lse; split requests get fp32 partials (unnormalised
  * output, then reference max and running sum) in the workspace, merged by s2l_split_reduce.

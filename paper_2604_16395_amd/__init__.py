@@ -26,7 +26,7 @@ __all__ = ["PagedKVCache", "Batch", "plan_opts", "S2LError", "S2LLibraryMissing"
            "s2l_abi_version", "s2l_kv_append", "s2l_kv_gather", "s2l_kv_swap_out", "s2l_kv_swap_in",
            "s2l_check_tables", "s2l_append_chunk_prefill_attn", "s2l_calib_stream_read", "s2l_calib_mfma_bf16", "s2l_attn_workspace_bytes",
            "s2l_attn_plan", "s2l_chunk_prefill_attn", "s2l_chunk_prefill_attn_q8", "s2l_attn_main", "s2l_split_reduce",
-           "s2l_plan_host", "library_path", "plan_status"]
+           "s2l_plan_host", "library_path", "plan_status", "s2l_chunk_prefill_attn_noalloc"]
 
 HEAD_DIM = 128
 PAGE_SIZE = 16
@@ -260,6 +260,22 @@ def s2l_append_chunk_prefill_attn(cache, batch, k_new, v_new, q, num_q_heads, so
               _ptr(q), num_q_heads, float(softmax_scale), _ptr(out), _ptr(lse), ctypes.byref(plan),
               _ptr(workspace), workspace.numel(), ctypes.byref(fused), _stream(stream))
     return bool(fused.value)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20     # S2L_NOALLOC_SCRATCH_BYTES of include/s2l.h
+
+
+def s2l_chunk_prefill_attn_noalloc(cache, batch, q, num_q_heads, softmax_scale, out, lse, opts=None, stream=None):
+    """Plan + attention + merge with the library's own scratch (no workspace, no allocation);
+    returns the plan's s2l_plan_info.  Calls overlapping on one GPU race (shared scratch)."""
+    _check(q, torch.bfloat16, "q")
+    _check(out, torch.bfloat16, "out")
+    _check(lse, torch.float32, "lse")
+    info = s2l_plan_info()
+    cc, bc = cache.c(), batch.c()
+    _lib.call("s2l_chunk_prefill_attn_noalloc", ctypes.byref(cc), ctypes.byref(bc), _ptr(q), num_q_heads,
+              float(softmax_scale), _ptr(out), _ptr(lse), _opts_ptr(opts), ctypes.byref(info), _stream(stream))
+    return info
 
 
 def s2l_attn_main(cache, batch, q, num_q_heads, softmax_scale, out, lse, plan, workspace, stream=None):

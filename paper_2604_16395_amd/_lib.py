@@ -97,6 +97,8 @@ SIGNATURES = {
                                        c_vp, ctypes.c_size_t, c_vp]),
     "s2l_append_chunk_prefill_attn": (c_i32, [P_cache, P_batch, c_vp, c_vp, c_vp, c_i32, ctypes.c_float, c_vp,
                                               c_vp, P_info, c_vp, ctypes.c_size_t, P_i32, c_vp]),
+    "s2l_chunk_prefill_attn_noalloc": (c_i32, [P_cache, P_batch, c_vp, c_i32, ctypes.c_float, c_vp, c_vp, P_opts,
+                                               P_info, c_vp]),
     "s2l_attn_main": (c_i32, [P_cache, P_batch, c_vp, c_i32, ctypes.c_float, c_vp, c_vp, P_info,
                               c_vp, ctypes.c_size_t, c_vp]),
     "s2l_split_reduce": (c_i32, [P_batch, c_i32, c_vp, c_vp, P_info, c_vp, ctypes.c_size_t, c_vp]),

@@ -610,6 +610,43 @@ s2l_status s2l_chunk_prefill_attn_q8(const s2l_kv_cache* cache, const s2l_batch*
   return s2l_split_reduce(batch, num_q_heads, out, lse, plan, workspace, ws_bytes, stream);
 }
 
+s2l_status s2l_chunk_prefill_attn_noalloc(const s2l_kv_cache* cache, const s2l_batch* batch, const void* q,
+                                          int32_t num_q_heads, float softmax_scale, void* out, float* lse,
+                                          const s2l_plan_opts* opts, s2l_plan_info* plan_out, void* stream) {
+  s2l_status st;
+  int64_t T = 0;
+  if ((st = check_cache(cache, batch)) != S2L_OK) return st;
+  if ((st = check_batch(batch, true, &T)) != S2L_OK) return st;
+  if ((st = check_heads(num_q_heads, cache->num_kv_heads)) != S2L_OK) return st;
+  if (!(softmax_scale > 0.0f) || !std::isfinite(softmax_scale))
+    return fail(S2L_EINVAL, "softmax_scale must be finite and > 0");
+  if (T > 0 && (!q || !out)) return fail(S2L_EINVAL, "q/out is NULL");
+  Resolved o;
+  if ((st = resolve_opts(opts, true, 0, batch->num_reqs, batch->chunk_lens_host, num_q_heads, cache->num_kv_heads,
+                         &o)) != S2L_OK)
+    return st;
+  s2l_plan_info pi;
+  host_plan(batch->num_reqs, batch->prefix_lens_host, batch->chunk_lens_host, num_q_heads, cache->num_kv_heads, o,
+            &pi, nullptr, 0);
+  if (pi.workspace_bytes > (int64_t)s2l::kNoAllocScratchBytes)
+    return fail(S2L_EWORKSPACE,
+                "this batch needs %lld bytes of workspace, more than the %zu bytes of scratch the allocation-free "
+                "call holds; use s2l_chunk_prefill_attn with a caller workspace",
+                (long long)pi.workspace_bytes, s2l::kNoAllocScratchBytes);
+  void* ws = nullptr;
+  hipError_t e = s2l::noalloc_scratch(&ws);
+  if (e != hipSuccess) return hip_fail("taking the scratch array's device address", e);
+  s2l_plan_info info;
+  if ((st = s2l_attn_plan(batch, num_q_heads, cache->num_kv_heads, opts, ws, s2l::kNoAllocScratchBytes, &info,
+                          stream)) != S2L_OK)
+    return st;
+  if ((st = s2l_chunk_prefill_attn(cache, batch, q, num_q_heads, softmax_scale, out, lse, &info, ws,
+                                   s2l::kNoAllocScratchBytes, stream)) != S2L_OK)
+    return st;
+  if (plan_out) *plan_out = info;
+  return ok();
+}
+
 s2l_status s2l_plan_host(int32_t num_reqs, const int32_t* prefix_lens_host, const int32_t* chunk_lens_host,
                          int32_t num_q_heads, int32_t num_kv_heads, const s2l_plan_opts* opts, int32_t num_cus,
                          s2l_plan_info* info, int32_t* items_out, int64_t item_capacity) {

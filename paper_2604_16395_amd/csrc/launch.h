@@ -90,4 +90,9 @@ struct ReduceLaunch {
 };
 hipError_t launch_split_reduce(const ReduceLaunch& a, hipStream_t stream);
 
+// Size of the library-held scratch array of the allocation-free attention call, and its
+// device address on the current device (taken on the first call there; noalloc.hip).
+constexpr size_t kNoAllocScratchBytes = (size_t)64 << 20;
+hipError_t noalloc_scratch(void** ptr);
+
 }  // namespace s2l

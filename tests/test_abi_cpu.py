@@ -195,3 +195,16 @@ def test_append_and_attention_checks_every_argument_before_enqueueing():
     assert call(kn=None) == _lib.S2L_EINVAL
     assert call(nbytes=ok_bytes - 1) == _lib.S2L_EWORKSPACE
     assert fused.value == -1                       # nothing decided, nothing enqueued
+
+
+def test_noalloc_call_rejects_a_plan_larger_than_its_scratch():
+    """16 pieces of a 512-token chunk with 32 query heads need 138 MB of partials: more than
+    the 64 MiB scratch of the allocation-free call; rejected on the host, nothing launched."""
+    b, _keep = _batch([8192], [512], max_pages=1024)
+    c = _cache(hkv=8)
+    o = _lib.s2l_plan_opts(target_items=1 << 20, min_split_keys=64, max_splits=16)
+    info = _lib.s2l_plan_info()
+    st = _lib.lib().s2l_chunk_prefill_attn_noalloc(ctypes.byref(c), ctypes.byref(b), FAKE, 32, 0.088, FAKE, None,
+                                                   ctypes.byref(o), ctypes.byref(info), None)
+    assert st == _lib.S2L_EWORKSPACE
+    assert b"allocation-free" in _lib.lib().s2l_last_error()
