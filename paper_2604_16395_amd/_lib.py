@@ -8,7 +8,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libs2l.so")
+# S2L_LIBRARY selects another build of the same library (the host-sanitizer build of
+# `python -m paper_2604_16395_amd.build --sanitize`); by default the in-tree libs2l.so.
+LIB_PATH = os.environ.get("S2L_LIBRARY") or os.path.join(_HERE, "libs2l.so")
 
 S2L_OK, S2L_EINVAL, S2L_ERANGE, S2L_EWORKSPACE, S2L_ENOTSUP, S2L_EHIP = 0, -1, -2, -3, -4, -5
 S2L_KV_BF16, S2L_KV_FP8_E4M3 = 0, 1

@@ -1,6 +1,12 @@
 """Build libs2l.so (HIP kernels for gfx950 + the C-ABI layer) in place.
 
-Usage: python -m paper_2604_16395_amd.build [-v]
+Usage: python -m paper_2604_16395_amd.build [-v] [--sanitize]
+
+--sanitize also builds _build/san/libs2l.so: the same device objects, with the host C++
+(argument validation, the host planner, the scheduler) compiled by g++ under AddressSanitizer
+and UndefinedBehaviorSanitizer.  Load it with S2L_LIBRARY=<path> and the ASan runtime first in
+LD_PRELOAD (tests/test_sanitize_cpu.py runs the host-side test files that way); it is for the
+CPU tests, not for GPU runs.
 """
 import concurrent.futures
 import glob
@@ -63,5 +69,39 @@ def build(verbose=False):
     return LIB
 
 
+SAN = os.path.join(BUILD, "san")
+SAN_LIB = os.path.join(SAN, "libs2l.so")
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer"]
+
+
+def build_sanitized(verbose=False):
+    """Host sources under ASan + UBSan (g++), linked with the device objects of build()."""
+    build(verbose)
+    os.makedirs(SAN, exist_ok=True)
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(_hipcc())))
+    gxx = os.environ.get("CXX") or shutil.which("g++")
+    if not gxx:
+        raise RuntimeError("g++ not found")
+    objs = []
+    for src in sorted(glob.glob(os.path.join(CSRC, "*.cpp"))):
+        obj = os.path.join(SAN, os.path.basename(src) + ".o")
+        cmd = [gxx, "-std=c++17", "-O1", "-g", "-fPIC", *SAN_FLAGS, "-D__HIP_PLATFORM_AMD__",
+               "-I", os.path.join(rocm, "include"), "-I", INCLUDE, "-I", CSRC, "-c", src, "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        subprocess.run(cmd, check=True)
+        objs.append(obj)
+    dev = sorted(glob.glob(os.path.join(BUILD, "*.hip.o")))
+    lib_dir = os.path.join(rocm, "lib")
+    cmd = [gxx, "-shared", *SAN_FLAGS, "-o", SAN_LIB, *dev, *objs, "-L", lib_dir, "-lamdhip64",
+           f"-Wl,-rpath,{lib_dir}"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+    return SAN_LIB
+
+
 if __name__ == "__main__":
     print(build(verbose="-v" in sys.argv))
+    if "--sanitize" in sys.argv:
+        print(build_sanitized(verbose="-v" in sys.argv))
