@@ -110,7 +110,7 @@ class Setup:
                    self.case.v_scale)
         self.appended = True
 
-    def attention(self, opts=None, with_lse=True, use_main_and_reduce=False, q8=False):
+    def attention(self, opts=None, with_lse=True, use_main_and_reduce=False, q8=False, scale=SCALE):
         c = self.case
         T, hq = c.total_tokens, c.num_q_heads
         nbytes = s2l.s2l_attn_workspace_bytes(self.batch, hq, c.num_kv_heads, opts)
@@ -120,17 +120,17 @@ class Setup:
         out = torch.full((T, hq, 128), float("nan"), dtype=torch.bfloat16, device=DEV)
         lse = torch.full((T, hq), float("nan"), dtype=torch.float32, device=DEV) if with_lse else None
         if q8:
-            s2l.s2l_chunk_prefill_attn_q8(self.cache, self.batch, self.q, hq, SCALE, out, lse, plan, ws)
+            s2l.s2l_chunk_prefill_attn_q8(self.cache, self.batch, self.q, hq, scale, out, lse, plan, ws)
         elif use_main_and_reduce:
-            s2l.s2l_attn_main(self.cache, self.batch, self.q, hq, SCALE, out, lse, plan, ws)
+            s2l.s2l_attn_main(self.cache, self.batch, self.q, hq, scale, out, lse, plan, ws)
             s2l.s2l_split_reduce(self.batch, hq, out, lse, plan, ws)
         else:
-            s2l.s2l_chunk_prefill_attn(self.cache, self.batch, self.q, hq, SCALE, out, lse, plan, ws)
+            s2l.s2l_chunk_prefill_attn(self.cache, self.batch, self.q, hq, scale, out, lse, plan, ws)
         torch.cuda.synchronize()
         self.plan = plan
         return out, lse
 
-    def oracle(self, sample_rows=None, q8=False, spread=True):
+    def oracle(self, sample_rows=None, q8=False, spread=True, scale=SCALE):
         """(O, LSE, A, B): the oracle's output, log-sum-exp and the softmax-weighted means of
         |V| and of |V - O|.  q8: of the queries quantised per (token, head) row to e4m3.
         spread=False skips B (NaN), which costs a pass over |V_j - O| for every key: the
@@ -140,14 +140,14 @@ class Setup:
         key = None
         if self.named and self.appended:
             rows_key = None if sample_rows is None else tuple((r, tuple(v)) for r, v in sorted(sample_rows.items()))
-            key = (c.name, q8, rows_key, spread)
+            key = (c.name, q8, rows_key, spread, scale)
             if key in _ORACLE:
                 return _ORACLE[key]
         q = bf16_bits_to_f32(c.q_bits).astype(np.float64)
         if q8:
             q = quantize_rows(bf16_bits_to_f32(c.q_bits))[2]
         res = ref_batch_attn(q, self.kp_ref, self.vp_ref, self.tables, c.prefix_lens, c.chunk_lens,
-                             c.cu_chunk, c.num_q_heads, SCALE, c.kv_dtype, c.k_scale, c.v_scale,
+                             c.cu_chunk, c.num_q_heads, scale, c.kv_dtype, c.k_scale, c.v_scale,
                              sample_rows=sample_rows, with_abs=True, spread=spread)
         if key is not None:
             _ORACLE[key] = res
