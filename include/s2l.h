@@ -143,11 +143,12 @@ typedef struct s2l_plan_info {
 } s2l_plan_info;
 #define S2L_PLAN_UNIFORM 1
 
-/* ABI version (S2L_ABI_VERSION of the built library). */
+/* ABI version (S2L_ABI_VERSION of the built library).  An ABI utility, not a step of the
+ * method. */
 int32_t s2l_abi_version(void);
 
 /* Reason for the last failure on the calling thread ("" if none); valid until the next
- * call on this thread. */
+ * call on this thread.  An ABI utility, not a step of the method. */
 const char* s2l_last_error(void);
 
 /*
@@ -180,7 +181,8 @@ s2l_status s2l_kv_gather(const s2l_kv_cache* cache, const s2l_batch* batch, int3
                          const int32_t* cu_out, void* k_out, void* v_out, void* stream);
 
 /*
- * Validation of block-table contents on the device, a debugging aid: the other calls assume
+ * Validation of block-table contents on the device (the block tables of Sec. 2.2's paged
+ * cache), a debugging aid: the other calls assume
  * the used entries are valid page ids and do not check them.  Counts the used entries of
  * every request (logical pages 0 .. ceil((P + C) / 16) - 1) that lie outside
  * [0, cache->num_pages).
@@ -330,7 +332,9 @@ s2l_status s2l_chunk_prefill_attn_noalloc(const s2l_kv_cache* cache, const s2l_b
                                           const s2l_plan_opts* opts, s2l_plan_info* plan_out, void* stream);
 
 /*
- * The main attention kernel alone (online softmax over the work items of the plan).
+ * The main attention kernel alone: the prefill attention of Sec. 2.1 over the paged cache of
+ * Sec. 2.2 (online softmax over the work items of the plan).  Running it and
+ * s2l_split_reduce as two launches is this library's choice, not the paper's.
  * Unsplit requests get their final out/lse; split requests get fp32 partials (unnormalised
  * output, then reference max and running sum) in the workspace, merged by s2l_split_reduce.
  */
@@ -340,7 +344,9 @@ s2l_status s2l_attn_main(const s2l_kv_cache* cache, const s2l_batch* batch,
                          void* workspace, size_t ws_bytes, void* stream);
 
 /*
- * Log-sum-exp merge of split partials (online-softmax merge): for each row and head of a
+ * Log-sum-exp merge of split partials (the standard online-softmax merge; no passage of the
+ * paper describes it: it completes the exact softmax of Sec. 2.1 over key ranges that were
+ * processed apart).  For each row and head of a
  * split request, m* = max_s m_s, l* = sum_s l_s 2^(m_s - m*), out = sum_s acc_s 2^(m_s - m*) / l*
  * (bf16), lse = ln(2) (m* + log2 l*) (m in the log2 domain).  Enqueues nothing when the
  * plan has no split request.
@@ -350,7 +356,8 @@ s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* o
                             void* stream);
 
 /*
- * Host-only view of the partition (no GPU needed): fills, for each request, the number of
+ * Host-only view of the partition of a scheduler step's batch (Sec. 4.1; no GPU needed), for
+ * tests and sizing: fills, for each request, the number of
  * query tiles and of key-range pieces, and the workspace layout, exactly as s2l_attn_plan
  * would store them.  items_out, if not NULL, receives num_items rows of 8 int32:
  * {request, kv_head, token_begin, token_end, key_begin, key_end, piece, num_pieces};
@@ -361,8 +368,8 @@ s2l_status s2l_plan_host(int32_t num_reqs, const int32_t* prefix_lens_host, cons
                          int32_t num_cus, s2l_plan_info* info, int32_t* items_out, int64_t item_capacity);
 
 /*
- * Measurement support (not part of the attention path): ceilings measured on the GPU at
- * hand, for reporting the kernels against.
+ * Measurement support (not part of the attention path, and not in the paper): ceilings
+ * measured on the GPU at hand, for reporting the kernels against.
  *   s2l_calib_stream_read: one streaming read of `bytes` (device, a multiple of 16, > 0)
  *     by `grid` workgroups of 256 threads; each thread writes one word of `sink` (device,
  *     grid * 256 uint32).  Bytes read / kernel time = reachable HBM read bandwidth.

@@ -148,27 +148,33 @@ int32_t s2l_lcp_len(const int32_t* a, int32_t na, const int32_t* b, int32_t nb);
 s2l_status s2l_sched_create(const s2l_sched_config* cfg, s2l_sched** out);
 void s2l_sched_destroy(s2l_sched* s);
 
-/* A new request with `n` input tokens (n >= 0) arriving at time `now` (seconds, any
+/* new_stream (Sec. 5.1; lifecycle of Sec. 4.2): a new request with `n` input tokens (n >= 0)
+ * arriving at time `now` (seconds, any
  * origin, non-decreasing over calls).  req_id must be new.  S2L_ERANGE if the input
  * needs more than max_blocks_per_req blocks. */
 s2l_status s2l_sched_new_stream(s2l_sched* s, int64_t req_id, const int32_t* ids, int32_t n,
                                 int32_t input_complete, double now);
-/* Append mode: n more tokens after the current input.  The request must be unfinished
+/* Append mode (Sec. 4.2, Sec. 5.1): n more tokens after the current input.  The request must
+ * be unfinished
  * with its input not yet complete. */
 s2l_status s2l_sched_append(s2l_sched* s, int64_t req_id, const int32_t* ids, int32_t n,
                             int32_t input_complete, double now);
-/* Update mode: the input becomes ids[0..n); LCP invalidation as above.  *lcp_out (may be
+/* Update mode (Sec. 4.2): the input becomes ids[0..n); LCP invalidation as above.  *lcp_out
+ * (may be
  * NULL) receives the LCP length. */
 s2l_status s2l_sched_update(s2l_sched* s, int64_t req_id, const int32_t* ids, int32_t n,
                             int32_t input_complete, double now, int32_t* lcp_out);
-/* One scheduling step: finish completed requests, phase 1, phase 2.  The scheduled
+/* One scheduling step (Sec. 4.1; preemption by Sec. 4.3's cost model): finish completed
+ * requests, phase 1, phase 2.  The scheduled
  * requests' computed tokens advance by their chunk lengths (the caller runs the step). */
 s2l_status s2l_sched_step(s2l_sched* s, s2l_sched_step_out* out);
 
-/* The current priority order of the unfinished requests (ids into `ids`, at most `cap`;
+/* The current priority order of the unfinished requests under the configured policy
+ * (Sec. 4.4; its sorting time is what Sec. 6.5 reports) (ids into `ids`, at most `cap`;
  * *n = the number of unfinished requests; *order_ns = host time of the ordering). */
 s2l_status s2l_sched_priority_order(s2l_sched* s, int64_t* ids, int32_t cap, int32_t* n, int64_t* order_ns);
-/* One request's state; gpu_blocks / cpu_blocks (each [max_blocks_per_req], may be NULL)
+/* One request's state (the per-request bookkeeping of Sec. 4.1-4.3: computed tokens, held
+ * GPU and CPU blocks); gpu_blocks / cpu_blocks (each [max_blocks_per_req], may be NULL)
  * receive its block lists. */
 s2l_status s2l_sched_request(const s2l_sched* s, int64_t req_id, s2l_sched_req_info* info,
                              int32_t* gpu_blocks, int32_t* cpu_blocks);
