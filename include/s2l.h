@@ -137,11 +137,16 @@ typedef struct s2l_plan_info {
   int32_t key_halves;      /* wave groups per work item (1 or 2)                            */
   int32_t flags;           /* S2L_PLAN_UNIFORM: the items' key ranges are within 25% of     */
                            /* their mean, so consecutive items (one kv head's pages) are    */
-                           /* grouped onto one XCD's L2; otherwise items run longest        */
-                           /* request first, spread over the XCDs, so the dispatcher        */
-                           /* balances them                                                 */
+                           /* grouped onto one XCD's L2.  S2L_PLAN_BINNED: items of unequal */
+                           /* cost, each (request, kv head) group placed whole on the XCD   */
+                           /* with the least work so far, longest request first; the bins   */
+                           /* are padded with no-op items to equal length (num_items counts */
+                           /* them).  Otherwise (the bins would not balance to within 4%)   */
+                           /* items run longest request first, spread over the XCDs, so the */
+                           /* dispatcher balances them                                      */
 } s2l_plan_info;
 #define S2L_PLAN_UNIFORM 1
+#define S2L_PLAN_BINNED 2
 
 /* ABI version (S2L_ABI_VERSION of the built library).  An ABI utility, not a step of the
  * method. */
@@ -360,7 +365,8 @@ s2l_status s2l_split_reduce(const s2l_batch* batch, int32_t num_q_heads, void* o
  * tests and sizing: fills, for each request, the number of
  * query tiles and of key-range pieces, and the workspace layout, exactly as s2l_attn_plan
  * would store them.  items_out, if not NULL, receives num_items rows of 8 int32:
- * {request, kv_head, token_begin, token_end, key_begin, key_end, piece, num_pieces};
+ * {request, kv_head, token_begin, token_end, key_begin, key_end, piece, num_pieces}, the
+ * items in request order, then (binned plans) the bins' no-op padding as rows {-1, 0, ...};
  * item_capacity is its row count.  num_cus stands in for the device's CU count.
  */
 s2l_status s2l_plan_host(int32_t num_reqs, const int32_t* prefix_lens_host, const int32_t* chunk_lens_host,

@@ -362,5 +362,5 @@ if __name__ == "__main__":
     import sys
     g = torch.Generator(device="cuda")
     g.manual_seed(2024)
-    fn = {"decode_64x32k": decode_64x32k, "config2": cfg2, "config5": cfg5}[sys.argv[1]]
+    fn = {"decode_64x32k": decode_64x32k, "config2": cfg2, "config4": cfg4, "config5": cfg5}[sys.argv[1]]
     print(json.dumps(fn(torch.cuda.Stream(), g)), flush=True)

@@ -264,6 +264,34 @@ void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_
   }
   const bool uniform = n_items > 0 && keys_max * n_items <= keys_sum + keys_sum / 4;
   info->flags = uniform ? S2L_PLAN_UNIFORM : 0;
+  // binned order (plan_rules.h) for batches of items of unequal cost, when its bins balance
+  if (!uniform && n_items > 0 && R <= s2l::kBinnedMaxReqs && (int64_t)R * hkv <= s2l::kBinnedMaxGroups) {
+    std::vector<int32_t> order(R);
+    for (int32_t r = 0; r < R; ++r) order[r] = r;
+    auto key = [&](int32_t r) { return C[r] > 0 ? P[r] + C[r] : -1; };   // the device plan's ranking
+    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return key(a) > key(b); });
+    s2l::XcdBins bins;
+    s2l::bins_init(&bins);
+    for (int32_t r : order) {
+      const int32_t ns = s2l::req_splits(P[r], C[r], split_keys, o.max_splits);
+      const int32_t n = s2l::num_qtiles(C[r], tq) * ns;
+      const int64_t cost = s2l::group_cost(P[r], C[r], tq, ns);
+      int32_t pos;
+      for (int32_t gg = 0; gg < hkv; ++gg) s2l::bins_place(&bins, cost, n, &pos);
+    }
+    if (s2l::bins_balanced(bins)) {
+      const int64_t padded = (int64_t)s2l::kNumXcds * s2l::bins_len(bins);
+      if (items)   // the rows past the real items are the bins' no-op padding
+        for (int64_t k = n_items; k < padded && k < cap; ++k) {
+          int32_t* row = items + 8 * k;
+          row[0] = -1;
+          for (int j = 1; j < 8; ++j) row[j] = 0;
+        }
+      info->num_items = (int32_t)padded;
+      info->workspace_bytes = s2l::plan_layout(R, padded, n_tiles, part).end;
+      info->flags = S2L_PLAN_BINNED;
+    }
+  }
 }
 
 s2l::PlanDims plan_dims(const s2l_plan_info* p) {
@@ -328,7 +356,7 @@ s2l_status attn_launch(const s2l_kv_cache* cache, const s2l_batch* batch, const 
   a.dims = plan_dims(plan);
   a.tile_cols = plan->tile_cols;
   a.key_halves = plan->key_halves;
-  a.group_by_xcd = (plan->flags & S2L_PLAN_UNIFORM) != 0;
+  a.group_by_xcd = (plan->flags & (S2L_PLAN_UNIFORM | S2L_PLAN_BINNED)) != 0;
   a.knew = k_new;
   a.vnew = v_new;
   a.q8 = q8;
@@ -524,6 +552,7 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
   a.split_keys = pi.split_keys;
   a.max_splits = o.max_splits;
   a.tile_cols = o.tile_cols;
+  a.binned = (pi.flags & S2L_PLAN_BINNED) != 0;
   a.ws_bytes = (int64_t)ws_bytes;
   a.workspace = workspace;
   (void)hipGetLastError();

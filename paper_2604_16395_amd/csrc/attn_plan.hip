@@ -14,6 +14,7 @@ constexpr int kPlanThreads = 256;
 constexpr int kPlanWaves = kPlanThreads / 64;
 constexpr int kLdsReqs = 1024;   // batches up to this size keep their per-request values in LDS
 constexpr int kRankReqs = kPlanThreads;   // batches up to this size are laid out longest first
+static_assert(kRankReqs == kBinnedMaxReqs, "the binned order needs the ranking");
 
 // Block-wide exclusive scan of N int64 values; returns the block totals in tot[].
 template <int N>
@@ -66,6 +67,8 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
       s_cu[kLdsReqs];
   __shared__ int64_t s_part[kLdsReqs];
   __shared__ int32_t s_key[kRankReqs], s_order[kRankReqs];
+  __shared__ int32_t s_gbin[kBinnedMaxGroups], s_gpos[kBinnedMaxGroups];   // binned order: bin, position
+  __shared__ int32_t s_bin_cnt[kNumXcds], s_bin_len;
   const int R = a.num_reqs;
   const int G = a.hq / a.hkv;
   const int tq = tile_tokens(G, a.tile_cols);
@@ -108,7 +111,6 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
   }
   block_scan<5>(v, excl, tot, sh);
   const int64_t num_items = tot[0], part_floats = tot[1], num_tiles = tot[2];
-  const bool fits = num_items <= pp.cap_items && num_tiles <= pp.cap_tiles && part_floats <= pp.cap_part_floats;
   int64_t items = excl[0], part = excl[1], tiles = excl[2];
   for (int k = k0; k < k1; ++k) {
     const int r = req_at(k);
@@ -134,6 +136,31 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     part += req_part_floats(ns, C, a.hq);
     tiles += (int64_t)a.hkv * nqt;
   }
+  // Binned order (plan_rules.h): (request, kv head) groups in ranked order, each to the XCD
+  // bin with the least work, on one thread (it is sequential; the plan runs once per step).
+  const bool binned = a.binned != 0 && ranked && R * a.hkv <= kBinnedMaxGroups;
+  int64_t records = num_items;
+  if (binned) {
+    __syncthreads();   // the slot-ordered request values are in LDS
+    if (threadIdx.x == 0) {
+      XcdBins b;
+      bins_init(&b);
+      for (int k = 0; k < R; ++k) {
+        const int ns = s_ns[k], n = num_qtiles(s_c[k], tq) * ns;
+        const int64_t cost = group_cost(s_p[k], s_c[k], tq, ns);
+        for (int gg = 0; gg < a.hkv; ++gg) {
+          int32_t pos;
+          s_gbin[k * a.hkv + gg] = bins_place(&b, cost, n, &pos);
+          s_gpos[k * a.hkv + gg] = pos;
+        }
+      }
+      for (int x = 0; x < kNumXcds; ++x) s_bin_cnt[x] = b.count[x];
+      s_bin_len = bins_len(b);
+    }
+    __syncthreads();
+    records = (int64_t)kNumXcds * s_bin_len;
+  }
+  const bool fits = records <= pp.cap_items && num_tiles <= pp.cap_tiles && part_floats <= pp.cap_part_floats;
   if (threadIdx.x == 0) {
     pp.item_off[R] = (int32_t)num_items;
     pp.cu[R] = a.cu_chunk[R];
@@ -145,7 +172,7 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     h->hkv = a.hkv;
     h->g = G;
     h->tq = tq;
-    h->num_items = fits ? (int32_t)num_items : 0;
+    h->num_items = fits ? (int32_t)records : 0;
     h->num_split_reqs = (int32_t)tot[3];
     h->split_keys = split_keys;
     h->status = fits ? 0 : 1;
@@ -157,24 +184,24 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
   if (!fits) return;
   __syncthreads();   // request arrays (global and LDS) complete
 
-  // one record per item; the request of item w is found by binary search over item offsets
-  for (int w = threadIdx.x; w < (int)num_items; w += kPlanThreads) {
-    int r, tile0, P, C, ns, row0, off;
+  // The record of item `local` of the request at ranked slot k (request-local items: kv head
+  // g, then query tile, then piece).
+  auto make_rec = [&](int k, int local) {
+    int r, tile0, P, C, ns, row0;
     int64_t part_off;
     if (R <= kLdsReqs) {
-      const int k = upper_index(s_item_off, R, w);
       r = s_req[k];
       tile0 = s_tile_off[k];
-      P = s_p[k], C = s_c[k], ns = s_ns[k], row0 = s_cu[k], off = s_item_off[k], part_off = s_part[k];
+      P = s_p[k], C = s_c[k], ns = s_ns[k], row0 = s_cu[k], part_off = s_part[k];
     } else {   // request order (no ranking above kRankReqs requests), offsets in global memory
-      r = upper_index(pp.item_off, R, w);
+      r = k;
       tile0 = 0;
-      for (int k = 0; k < r; ++k) tile0 += a.hkv * num_qtiles(a.chunk_lens[k], tq);
-      P = a.prefix_lens[r], C = a.chunk_lens[r], ns = pp.ns[r], row0 = a.cu_chunk[r], off = pp.item_off[r];
+      for (int j = 0; j < r; ++j) tile0 += a.hkv * num_qtiles(a.chunk_lens[j], tq);
+      P = a.prefix_lens[r], C = a.chunk_lens[r], ns = pp.ns[r], row0 = a.cu_chunk[r];
       part_off = pp.part_off[r];
     }
     const int nqt = num_qtiles(C, tq);
-    const Item it = decode_local(w - off, nqt, ns);
+    const Item it = decode_local(local, nqt, ns);
     ItemRec rec;
     rec.r = r;
     rec.g = it.g;
@@ -189,7 +216,30 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     rec.tile = tile0 + it.g * nqt + it.qt;
     rec.part_off = part_off;
     rec.pad0 = rec.pad1 = 0;
-    pp.items[w] = rec;
+    return rec;
+  };
+  if (binned) {
+    // each group's items at its place in its bin, then the bins' padding (request -1)
+    const int N = s_bin_len;
+    for (int q = threadIdx.x; q < R * a.hkv; q += kPlanThreads) {
+      const int k = q / a.hkv, gg = q % a.hkv;
+      const int n = num_qtiles(s_c[k], tq) * s_ns[k];
+      const int64_t base = (int64_t)s_gbin[q] * N + s_gpos[q];
+      for (int j = 0; j < n; ++j) pp.items[base + j] = make_rec(k, gg * n + j);
+    }
+    for (int w = threadIdx.x; w < kNumXcds * N; w += kPlanThreads)
+      if (w % N >= s_bin_cnt[w / N]) {
+        ItemRec rec = {};
+        rec.r = -1;
+        pp.items[w] = rec;
+      }
+    return;
+  }
+  // one record per item; the request of item w is found by binary search over item offsets
+  for (int w = threadIdx.x; w < (int)num_items; w += kPlanThreads) {
+    const int k = R <= kLdsReqs ? upper_index(s_item_off, R, w) : upper_index(pp.item_off, R, w);
+    const int off = R <= kLdsReqs ? s_item_off[k] : pp.item_off[k];
+    pp.items[w] = make_rec(k, w - off);
   }
 }
 

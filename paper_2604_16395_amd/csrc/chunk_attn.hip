@@ -195,7 +195,7 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     poison_outputs(out, lse, total_rows, hq);
     return;
   }
-  if (w_item >= W) return;
+  if (w_item >= W || it.r < 0) return;   // past the plan's items, or a bin's padding
   const int P = it.p, C = it.c, row0 = it.row0, ns = it.ns, g = it.g;
   const int i0 = it.i0, i1 = it.i1;
   const int G = hq / hkv;

@@ -89,7 +89,7 @@ __global__ __launch_bounds__(kDecodeWaves * 64, 1) void attn_decode_kernel(
     poison_outputs(out, lse, total_rows, hq);
     return;
   }
-  if (w_item >= pv.hdr->num_items) return;
+  if (w_item >= pv.hdr->num_items || it.r < 0) return;   // past the plan's items, or a bin's padding
   const int P = it.p, C = it.c, row0 = it.row0, ns = it.ns, g = it.g;
   const int i0 = it.i0, i1 = it.i1, lo = it.lo, hi = it.hi;
   const int G = hq / hkv;

@@ -43,6 +43,7 @@ struct PlanLaunch {
   const int32_t* cu_chunk;
   int32_t num_reqs, hq, hkv;
   int32_t split_keys, max_splits, tile_cols;   // split_keys chosen by the host planner
+  int32_t binned;                              // the host chose the binned item order
   int64_t ws_bytes;
   void* workspace;
 };

@@ -191,4 +191,72 @@ S2L_HD inline int32_t xcd_logical(int32_t b, int32_t n) {
   return x * per + (x < rem ? x : rem) + k;
 }
 
+// Binned item order, for batches whose items differ in cost.  The (request, kv head) groups,
+// requests longest first (by P + C; ties by index), each go whole to the XCD bin with the
+// least work so far (lowest index on ties), so that a group's K/V pages are read by one
+// L2; a bin's items then run in that order on its XCD.  Bins are padded with no-op records
+// (request -1) to the length N of the longest, so logical item x N + k is item k of bin x and
+// xcd_logical over 8 N workgroups sends bin x to XCD x.  Used when the bins' work is within
+// 4% of their mean; otherwise items keep the longest-request-first order over all XCDs.
+constexpr int kBinnedMaxReqs = 256;      // requests the device plan ranks
+constexpr int kBinnedMaxGroups = 4096;   // (request, kv head) groups the device plan bins
+constexpr int64_t kItemCostKeys = 192;   // a work item's fixed cost (prologue and tail), in keys
+
+// Work of one (request, kv head) group: the key ranges [0, P + i1) of its query tiles, plus
+// the fixed cost of each of its nqt x ns items.
+S2L_HD inline int64_t group_cost(int32_t p, int32_t c, int32_t tq, int32_t ns) {
+  const int32_t nqt = num_qtiles(c, tq);
+  int64_t k = 0;
+  for (int32_t qt = 0; qt < nqt; ++qt) {
+    const int32_t e = (qt + 1) * tq;
+    k += (int64_t)p + (e < c ? e : c);
+  }
+  return k + kItemCostKeys * nqt * ns;
+}
+
+struct XcdBins {
+  int64_t load[kNumXcds];
+  int32_t count[kNumXcds];
+};
+S2L_HD inline void bins_init(XcdBins* b) {
+  for (int x = 0; x < kNumXcds; ++x) {
+    b->load[x] = 0;
+    b->count[x] = 0;
+  }
+}
+// The bin with the least work (lowest index on ties) takes a group of n items costing `cost`;
+// returns the bin and sets *pos to the group's first position in it.
+S2L_HD inline int32_t bins_place(XcdBins* b, int64_t cost, int32_t n, int32_t* pos) {
+  // every index is a constant after unrolling, so the bins stay in registers on the device
+  int32_t x = 0;
+  int64_t least = b->load[0];
+#pragma unroll
+  for (int y = 1; y < kNumXcds; ++y)
+    if (b->load[y] < least) {
+      least = b->load[y];
+      x = y;
+    }
+#pragma unroll
+  for (int y = 0; y < kNumXcds; ++y)
+    if (y == x) {
+      *pos = b->count[y];
+      b->count[y] += n;
+      b->load[y] += cost;
+    }
+  return x;
+}
+S2L_HD inline int32_t bins_len(const XcdBins& b) {
+  int32_t n = 0;
+  for (int x = 0; x < kNumXcds; ++x) n = b.count[x] > n ? b.count[x] : n;
+  return n;
+}
+S2L_HD inline bool bins_balanced(const XcdBins& b) {
+  int64_t sum = 0, mx = 0;
+  for (int x = 0; x < kNumXcds; ++x) {
+    sum += b.load[x];
+    mx = b.load[x] > mx ? b.load[x] : mx;
+  }
+  return sum > 0 && mx * kNumXcds * 25 <= sum * 26;
+}
+
 }  // namespace s2l

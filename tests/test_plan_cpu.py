@@ -10,6 +10,8 @@ import pytest
 from paper_2604_16395_amd import plan_opts, s2l_plan_host
 import workloads
 
+UNIFORM, BINNED = 1, 2
+
 
 def _coverage(P, C, hq, hkv, items, tile_cols):
     G = hq // hkv
@@ -52,11 +54,17 @@ def test_items_cover_each_visible_pair_once(target, hq, hkv, tile_cols, halves):
                                                          tile_cols=tile_cols, key_halves=halves),
                                 with_items=True)
     assert info.num_items == len(items)
+    real, pad = items[items[:, 0] >= 0], items[items[:, 0] < 0]
+    assert np.all(pad == [-1, 0, 0, 0, 0, 0, 0, 0])            # no-op padding of the XCD bins
+    if info.flags & BINNED:
+        assert info.num_items % 8 == 0 and len(pad) < info.num_items
+    else:
+        assert len(pad) == 0
     assert tile_cols == 0 or info.tile_cols == tile_cols
-    _coverage(P, C, hq, hkv, items, info.tile_cols)
+    _coverage(P, C, hq, hkv, real, info.tile_cols)
     assert info.total_tokens == C.sum()
     # one tile per (request, kv head, query tile); the items of a tile are its pieces
-    assert info.num_tiles == len({(r, g, i0) for r, g, i0 in items[:, 0:3]})
+    assert info.num_tiles == len({(r, g, i0) for r, g, i0 in real[:, 0:3]})
 
 
 def test_plan_is_deterministic_and_independent_of_call():
@@ -160,3 +168,49 @@ def test_uniform_items_flag():
     P, C, _ = workloads.config4_lengths()
     info, _ = s2l_plan_host(P, C, 32, 8, num_cus=256)
     assert not (info.flags & 1)
+
+
+def _binned_len(P, C, hq, hkv, info, items):
+    """A second statement of the binned order's rule: (request, kv head) groups, requests by
+    P + C descending (ties by index, requests without new tokens last), each to the bin with the
+    least work so far (lowest index on ties); work of a group = the key ranges [0, P + i1) of its
+    query tiles + 192 keys per item.  Returns (bins balanced within 4%, padded item count)."""
+    tq = info.tile_cols // (hq // hkv)
+    real = items[items[:, 0] >= 0]
+    order = sorted(range(len(P)), key=lambda r: (-(P[r] + C[r] if C[r] > 0 else -1), r))
+    load, count = [0] * 8, [0] * 8
+    for r in order:
+        mine = real[(real[:, 0] == r) & (real[:, 1] == 0)]
+        n = len(mine)
+        cost = sum(int(P[r]) + min(t + tq, int(C[r])) for t in range(0, int(C[r]), tq)) + 192 * n
+        for _ in range(hkv):
+            x = min(range(8), key=lambda y: (load[y], y))
+            load[x] += cost
+            count[x] += n
+    return max(load) * 8 * 25 <= sum(load) * 26, 8 * max(count)
+
+
+@pytest.mark.parametrize("which", ["config2", "config4", "ragged", "uniform"])
+def test_binned_order_follows_its_rule(which):
+    if which == "config2":
+        P, C, _ = workloads.config2_lengths()
+    elif which == "config4":
+        P, C, _ = workloads.config4_lengths()
+    elif which == "ragged":
+        rng = np.random.default_rng(3)
+        P, C = rng.integers(0, 20000, 40), rng.integers(1, 700, 40)
+    else:
+        P, C = np.full(8, 4096), np.full(8, 512)
+    P, C = np.asarray(P, np.int32), np.asarray(C, np.int32)
+    info, items = s2l_plan_host(P, C, 32, 8, num_cus=256, with_items=True)
+    real = items[items[:, 0] >= 0]
+    if info.flags & UNIFORM:
+        assert which == "uniform" and len(real) == info.num_items
+        return
+    balanced, padded = _binned_len(P, C, 32, 8, info, items)
+    if balanced:
+        assert info.flags == BINNED and info.num_items == padded
+    else:
+        assert info.flags == 0 and info.num_items == len(real)
+    if which in ("config2", "config4"):
+        assert info.flags == BINNED   # the named mixed batches do balance
