@@ -207,6 +207,32 @@ int32_t choose_split_keys(int32_t R, const int32_t* P, const int32_t* C, int32_t
   return (int32_t)(hi * s2l::kKvTile);
 }
 
+// Binned item order (plan_rules.h): requests ranked as the device plan ranks them, their
+// (request, kv head) groups placed greedily.  Fills group_bin (if not NULL) by ranked slot and
+// kv head, sets *len to the longest bin's item count, and returns whether the bins balance.
+bool bin_groups(int32_t R, const int32_t* P, const int32_t* C, int32_t hkv, int32_t tq, int32_t split_keys,
+                int32_t max_splits, uint8_t* group_bin, int32_t* len) {
+  std::vector<int32_t> order(R);
+  for (int32_t r = 0; r < R; ++r) order[r] = r;
+  auto key = [&](int32_t r) { return C[r] > 0 ? P[r] + C[r] : -1; };
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return key(a) > key(b); });
+  s2l::XcdBins bins;
+  s2l::bins_init(&bins);
+  for (int32_t k = 0; k < R; ++k) {
+    const int32_t r = order[k];
+    const int32_t ns = s2l::req_splits(P[r], C[r], split_keys, max_splits);
+    const int32_t n = s2l::num_qtiles(C[r], tq) * ns;
+    const int64_t cost = s2l::group_cost(P[r], C[r], tq, ns);
+    for (int32_t gg = 0; gg < hkv; ++gg) {
+      int32_t pos;
+      const int32_t x = s2l::bins_place(&bins, cost, n, &pos);
+      if (group_bin) group_bin[k * hkv + gg] = (uint8_t)x;
+    }
+  }
+  *len = s2l::bins_len(bins);
+  return s2l::bins_balanced(bins);
+}
+
 // Host plan: the partition the device plan kernel stores (same rules, same order).
 void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_t hkv, const Resolved& o,
                s2l_plan_info* info, int32_t* items, int64_t cap) {
@@ -265,22 +291,10 @@ void host_plan(int32_t R, const int32_t* P, const int32_t* C, int32_t hq, int32_
   const bool uniform = n_items > 0 && keys_max * n_items <= keys_sum + keys_sum / 4;
   info->flags = uniform ? S2L_PLAN_UNIFORM : 0;
   // binned order (plan_rules.h) for batches of items of unequal cost, when its bins balance
+  int32_t bin_len = 0;
   if (!uniform && n_items > 0 && R <= s2l::kBinnedMaxReqs && (int64_t)R * hkv <= s2l::kBinnedMaxGroups) {
-    std::vector<int32_t> order(R);
-    for (int32_t r = 0; r < R; ++r) order[r] = r;
-    auto key = [&](int32_t r) { return C[r] > 0 ? P[r] + C[r] : -1; };   // the device plan's ranking
-    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return key(a) > key(b); });
-    s2l::XcdBins bins;
-    s2l::bins_init(&bins);
-    for (int32_t r : order) {
-      const int32_t ns = s2l::req_splits(P[r], C[r], split_keys, o.max_splits);
-      const int32_t n = s2l::num_qtiles(C[r], tq) * ns;
-      const int64_t cost = s2l::group_cost(P[r], C[r], tq, ns);
-      int32_t pos;
-      for (int32_t gg = 0; gg < hkv; ++gg) s2l::bins_place(&bins, cost, n, &pos);
-    }
-    if (s2l::bins_balanced(bins)) {
-      const int64_t padded = (int64_t)s2l::kNumXcds * s2l::bins_len(bins);
+    if (bin_groups(R, P, C, hkv, tq, split_keys, o.max_splits, nullptr, &bin_len)) {
+      const int64_t padded = (int64_t)s2l::kNumXcds * bin_len;
       if (items)   // the rows past the real items are the bins' no-op padding
         for (int64_t k = n_items; k < padded && k < cap; ++k) {
           int32_t* row = items + 8 * k;
@@ -553,6 +567,12 @@ s2l_status s2l_attn_plan(const s2l_batch* batch, int32_t num_q_heads, int32_t nu
   a.max_splits = o.max_splits;
   a.tile_cols = o.tile_cols;
   a.binned = (pi.flags & S2L_PLAN_BINNED) != 0;
+  if (a.binned) {
+    int32_t len;
+    const int32_t tq = s2l::tile_tokens(num_q_heads / num_kv_heads, o.tile_cols);
+    bin_groups(batch->num_reqs, batch->prefix_lens_host, batch->chunk_lens_host, num_kv_heads, tq, pi.split_keys,
+               o.max_splits, a.group_bin, &len);
+  }
   a.ws_bytes = (int64_t)ws_bytes;
   a.workspace = workspace;
   (void)hipGetLastError();

@@ -67,8 +67,8 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
       s_cu[kLdsReqs];
   __shared__ int64_t s_part[kLdsReqs];
   __shared__ int32_t s_key[kRankReqs], s_order[kRankReqs];
-  __shared__ int32_t s_gbin[kBinnedMaxGroups], s_gpos[kBinnedMaxGroups];   // binned order: bin, position
-  __shared__ int32_t s_bin_cnt[kNumXcds], s_bin_len;
+  __shared__ int64_t sh_bins[kNumXcds][kPlanWaves];
+  __shared__ int32_t s_bin_cnt[kNumXcds];
   const int R = a.num_reqs;
   const int G = a.hq / a.hkv;
   const int tq = tile_tokens(G, a.tile_cols);
@@ -136,29 +136,36 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     part += req_part_floats(ns, C, a.hq);
     tiles += (int64_t)a.hkv * nqt;
   }
-  // Binned order (plan_rules.h): (request, kv head) groups in ranked order, each to the XCD
-  // bin with the least work, on one thread (it is sequential; the plan runs once per step).
+  // Binned order (plan_rules.h): the host's bin of each (request, kv head) group, groups in
+  // ranked order; a block scan of the bins' item counts over contiguous segments of groups
+  // places every group's items in its bin.
   const bool binned = a.binned != 0 && ranked && R * a.hkv <= kBinnedMaxGroups;
+  const int ngroups = R * a.hkv;
+  const int gseg = (ngroups + kPlanThreads - 1) / kPlanThreads;
+  const int q0 = min(ngroups, (int)threadIdx.x * gseg), q1 = min(ngroups, q0 + gseg);
+  auto group_items = [&](int q) { const int k = q / a.hkv; return num_qtiles(s_c[k], tq) * s_ns[k]; };
+  int64_t bin_before[kNumXcds], bin_total[kNumXcds];
   int64_t records = num_items;
+  int bin_len = 0;
   if (binned) {
     __syncthreads();   // the slot-ordered request values are in LDS
-    if (threadIdx.x == 0) {
-      XcdBins b;
-      bins_init(&b);
-      for (int k = 0; k < R; ++k) {
-        const int ns = s_ns[k], n = num_qtiles(s_c[k], tq) * ns;
-        const int64_t cost = group_cost(s_p[k], s_c[k], tq, ns);
-        for (int gg = 0; gg < a.hkv; ++gg) {
-          int32_t pos;
-          s_gbin[k * a.hkv + gg] = bins_place(&b, cost, n, &pos);
-          s_gpos[k * a.hkv + gg] = pos;
-        }
-      }
-      for (int x = 0; x < kNumXcds; ++x) s_bin_cnt[x] = b.count[x];
-      s_bin_len = bins_len(b);
+    int64_t cnt[kNumXcds];
+#pragma unroll
+    for (int x = 0; x < kNumXcds; ++x) cnt[x] = 0;
+    for (int q = q0; q < q1; ++q) {
+      const int b = a.group_bin[q], n = group_items(q);
+#pragma unroll
+      for (int x = 0; x < kNumXcds; ++x) cnt[x] += x == b ? n : 0;
     }
-    __syncthreads();
-    records = (int64_t)kNumXcds * s_bin_len;
+    block_scan<kNumXcds>(cnt, bin_before, bin_total, sh_bins);
+#pragma unroll
+    for (int x = 0; x < kNumXcds; ++x) bin_len = max(bin_len, (int)bin_total[x]);
+    if (threadIdx.x < kNumXcds) {
+#pragma unroll
+      for (int x = 0; x < kNumXcds; ++x)
+        if (x == (int)threadIdx.x) s_bin_cnt[x] = (int)bin_total[x];
+    }
+    records = (int64_t)kNumXcds * bin_len;
   }
   const bool fits = records <= pp.cap_items && num_tiles <= pp.cap_tiles && part_floats <= pp.cap_part_floats;
   if (threadIdx.x == 0) {
@@ -219,12 +226,21 @@ __global__ __launch_bounds__(kPlanThreads) void attn_plan_kernel(PlanLaunch a, P
     return rec;
   };
   if (binned) {
-    // each group's items at its place in its bin, then the bins' padding (request -1)
-    const int N = s_bin_len;
-    for (int q = threadIdx.x; q < R * a.hkv; q += kPlanThreads) {
-      const int k = q / a.hkv, gg = q % a.hkv;
-      const int n = num_qtiles(s_c[k], tq) * s_ns[k];
-      const int64_t base = (int64_t)s_gbin[q] * N + s_gpos[q];
+    // this thread's groups at their places in their bins, then the bins' padding (request -1)
+    const int N = bin_len;
+    int64_t at[kNumXcds];
+#pragma unroll
+    for (int x = 0; x < kNumXcds; ++x) at[x] = bin_before[x];
+    for (int q = q0; q < q1; ++q) {
+      const int k = q / a.hkv, gg = q % a.hkv, b = a.group_bin[q], n = group_items(q);
+      int64_t pos = 0;
+#pragma unroll
+      for (int x = 0; x < kNumXcds; ++x)
+        if (x == b) {
+          pos = at[x];
+          at[x] += n;
+        }
+      const int64_t base = (int64_t)b * N + pos;
       for (int j = 0; j < n; ++j) pp.items[base + j] = make_rec(k, gg * n + j);
     }
     for (int w = threadIdx.x; w < kNumXcds * N; w += kPlanThreads)

@@ -44,6 +44,7 @@ struct PlanLaunch {
   int32_t num_reqs, hq, hkv;
   int32_t split_keys, max_splits, tile_cols;   // split_keys chosen by the host planner
   int32_t binned;                              // the host chose the binned item order
+  uint8_t group_bin[kBinnedMaxGroups];         // binned: XCD bin of group k Hkv + g (k = ranked slot)
   int64_t ws_bytes;
   void* workspace;
 };

@@ -197,9 +197,11 @@ S2L_HD inline int32_t xcd_logical(int32_t b, int32_t n) {
 // L2; a bin's items then run in that order on its XCD.  Bins are padded with no-op records
 // (request -1) to the length N of the longest, so logical item x N + k is item k of bin x and
 // xcd_logical over 8 N workgroups sends bin x to XCD x.  Used when the bins' work is within
-// 4% of their mean; otherwise items keep the longest-request-first order over all XCDs.
+// 4% of their mean; otherwise items keep the longest-request-first order over all XCDs.  The
+// host planner assigns the bins (it sizes the launch with them) and hands the device plan one
+// bin per group; the device places each group's items with a scan of the bins' item counts.
 constexpr int kBinnedMaxReqs = 256;      // requests the device plan ranks
-constexpr int kBinnedMaxGroups = 4096;   // (request, kv head) groups the device plan bins
+constexpr int kBinnedMaxGroups = 1024;   // (request, kv head) groups a plan launch carries bins for
 constexpr int64_t kItemCostKeys = 192;   // a work item's fixed cost (prologue and tail), in keys
 
 // Work of one (request, kv head) group: the key ranges [0, P + i1) of its query tiles, plus
