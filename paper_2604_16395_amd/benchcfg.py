@@ -325,11 +325,34 @@ def measured_ceilings(stream=None):
                    "register-only loop of 32x32x16 bf16 MFMAs, 8 waves per CU"}
 
 
+def prefix_sweep(stream, gen):
+    """The headline step's shape (one request, a 512-token chunk, 32q/8kv, bf16 pages) at prefixes
+    from 2K to 128K tokens: per-layer step (append, plan, attention, merge) and attention alone,
+    each over enough rotating layer pools to exceed the 256 MB last-level cache."""
+    rng = np.random.default_rng(1003)
+    out = []
+    for P in (2048, 4096, 8192, 16384, 32768, 65536, 131072):
+        pages = (P + 512 + 15) // 16
+        copies = int(min(32, max(2, math.ceil(512e6 / (pages * 8 * 16 * 128 * 2 * 2)))))
+        layer = Layer([P], [512], 32, 8, pages, tables_for([P], [512], pages, rng), gen, copies=copies)
+        us, attn_us, plan = measure_step(layer, stream, copies)
+        f = layer.flops()
+        out.append({"prefix": P, "layer_copies": copies, "us_per_step": round(us, 2), "attn_us": round(attn_us, 2),
+                    "attn_tflops": round(f / attn_us / 1e6, 1),
+                    "attn_pct_mfma_peak": round(100 * f / attn_us / 1e6 / PEAK_BF16_TFLOPS, 1),
+                    "work_items": plan.num_items})
+        del layer
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return {"workload": "one request, C = 512, 32q/8kv, bf16 KV, P from 2K to 128K", "points": out}
+
+
 def all_configs(seed=2024):
     """{config name: result or error string}; each config is measured independently."""
     stream = torch.cuda.Stream()
     res = {}
-    for name, fn in (("config2", cfg2), ("config3", cfg3), ("config4", cfg4), ("config5", cfg5)):
+    for name, fn in (("config2", cfg2), ("config3", cfg3), ("config4", cfg4), ("config5", cfg5),
+                     ("prefix_sweep", prefix_sweep)):
         gen = torch.Generator(device="cuda")
         gen.manual_seed(seed)
         try:
@@ -362,5 +385,6 @@ if __name__ == "__main__":
     import sys
     g = torch.Generator(device="cuda")
     g.manual_seed(2024)
-    fn = {"decode_64x32k": decode_64x32k, "config2": cfg2, "config4": cfg4, "config5": cfg5}[sys.argv[1]]
+    fn = {"decode_64x32k": decode_64x32k, "config2": cfg2, "config4": cfg4, "config5": cfg5,
+          "prefix_sweep": prefix_sweep}[sys.argv[1]]
     print(json.dumps(fn(torch.cuda.Stream(), g)), flush=True)
