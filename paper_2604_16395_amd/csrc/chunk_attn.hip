@@ -839,6 +839,54 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     l_fin = a0 * l_fin + a1 * ml1[1];
     m_fin = mstar;
   }
+  // Split piece, when the ring can hold the whole tile's rows (bf16 pages; one key group):
+  // the fp32 partial is staged through LDS, row-major with each row's 16-byte chunks
+  // permuted by (column mod 16) so that both the register-order writes and the row reads
+  // are free of bank conflicts, and then stored a row run at a time (the G head rows of a
+  // token are adjacent) with device-scope (sc1) stores, which write through the L2: no
+  // dirty partial lines are left for the write-back at the end of the launch.  The row sum
+  // and max follow with the same policy.
+  float* const acc = pv.partials + it.part_off;
+  const int64_t acc_bytes = (int64_t)ns * C * hq * (kHeadDim + 4) * 4;
+  if (kHalves == 1 && RingT::kBytes >= kColWaves * 32 * kHeadDim * 4 && ns > 1 && acc_bytes <= 0x7fffffff) {
+    constexpr int kSc1 = 16;   // cache policy: device scope
+    __builtin_amdgcn_s_barrier();   // every wave is past its last read of the ring
+    float* xs = reinterpret_cast<float*>(smem);
+#pragma unroll
+    for (int db = 0; db < 4; ++db)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<f32x4*>(xs + (col * 32 + ((8 * db + 2 * j + half) ^ (col & 15))) * 4) =
+            f32x4{o[db][4 * j] * v_mul, o[db][4 * j + 1] * v_mul, o[db][4 * j + 2] * v_mul,
+                  o[db][4 * j + 3] * v_mul};
+    wait_lgkmcnt0();
+    __builtin_amdgcn_s_barrier();
+    const auto prs = make_rsrc(acc, (int32_t)acc_bytes);
+    const int ncols = min(tq * G, (i1 - i0) * G);   // the valid columns of this tile
+    // row of column c: (s C + i0 + c / G) hq + g G + c % G = rbase + c + (c / G)(hq - G);
+    // c / G = (c ginv) >> 24 exactly for c < 256 and G < 2^16
+    const int64_t rbase = ((int64_t)it.s * C + i0) * hq + g * G;
+    const uint32_t ginv = ((1u << 24) + (uint32_t)G - 1) / (uint32_t)G;
+    constexpr int kThreads = kColWaves * 64;
+#pragma unroll
+    for (int u0 = 0; u0 < 32 * kColWaves * 32; u0 += kThreads) {
+      const int u = u0 + (int)threadIdx.x;
+      const int c = u >> 5, k = u & 31;   // column, 16-byte chunk
+      if (c < ncols) {
+        const f32x4 x = *reinterpret_cast<const f32x4*>(xs + (c * 32 + (k ^ (c & 15))) * 4);
+        const int64_t pr = rbase + c + (int64_t)(((uint32_t)c * ginv) >> 24) * (hq - G);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), prs, (uint32_t)(pr * 512 + 16 * k), 0,
+                                               kSc1);
+      }
+    }
+    if (valid && half == 0) {
+      const int64_t prow = ((int64_t)it.s * C + tok) * hq + hq_col;
+      const int64_t ml_off = (int64_t)ns * C * hq * kHeadDim * 4 + 16 * prow;
+      __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, f32x4{m_fin, l_fin, 0.f, 0.f}), prs,
+                                             (uint32_t)ml_off, 0, kSc1);
+    }
+    return;
+  }
   if (!valid) return;
   if (ns == 1) {
     const float inv = v_mul / l_fin;
@@ -854,9 +902,8 @@ __global__ __launch_bounds__(kColWaves * kHalves * 64, 8 / (kColWaves * kHalves)
     if (lse != nullptr && half == 0) lse[(int64_t)(row0 + tok) * hq + hq_col] = (m_fin + __log2f(l_fin)) * kLn2;
     return;
   }
-  // Split piece: fp32 partial (acc row, then (m, l, 0, 0)); a column with no visible key in
-  // this piece has (-inf, 0): the merge skips it.
-  float* acc = pv.partials + it.part_off;
+  // Split piece (other layouts): fp32 partial (acc row, then (m, l, 0, 0)), stored from the
+  // registers; a column with no visible key in this piece has (-inf, 0): the merge skips it.
   float* ml = acc + (int64_t)ns * C * hq * kHeadDim;
   const int64_t prow = ((int64_t)it.s * C + tok) * hq + hq_col;
   float* arow = acc + prow * kHeadDim + 4 * half;
