@@ -347,12 +347,38 @@ def prefix_sweep(stream, gen):
     return {"workload": "one request, C = 512, 32q/8kv, bf16 KV, P from 2K to 128K", "points": out}
 
 
+def tp_shares(stream, gen):
+    """One GPU's share of a tensor-parallel layer (the kv heads split over the GPUs, each with
+    its G query heads; attention needs no exchange): Llama-3-8B at TP = 2 (16q/4kv, bf16, the
+    headline step's P = 8192, C = 512) and Llama-3-70B at TP = 8 (8q/1kv, e4m3, config 5's
+    P = 131072, C = 2048), each over enough rotating layer pools to exceed the 256 MB cache."""
+    rng = np.random.default_rng(1007)
+    out = {}
+    for name, P, C, hq, hkv, fp8 in (("llama3_8b_tp2", 8192, 512, 16, 4, False),
+                                     ("llama3_70b_tp8", 131072, 2048, 8, 1, True)):
+        pages = (P + C + 15) // 16
+        per_copy = pages * hkv * 16 * 128 * 2 * (1 if fp8 else 2)
+        copies = int(min(32, max(2, math.ceil(512e6 / per_copy))))
+        layer = Layer([P], [C], hq, hkv, pages, tables_for([P], [C], pages, rng), gen, fp8=fp8, copies=copies)
+        us, attn_us, plan = measure_step(layer, stream, copies, reps=3)
+        f = layer.flops()
+        out[name] = {"prefix": P, "chunk": C, "heads": f"{hq}q/{hkv}kv", "kv": "e4m3" if fp8 else "bf16",
+                     "layer_copies": copies, "us_per_step": round(us, 2), "attn_us": round(attn_us, 2),
+                     "attn_tflops": round(f / attn_us / 1e6, 1),
+                     "attn_pct_mfma_peak": round(100 * f / attn_us / 1e6 / PEAK_BF16_TFLOPS, 1),
+                     "work_items": plan.num_items}
+        del layer
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    return out
+
+
 def all_configs(seed=2024):
     """{config name: result or error string}; each config is measured independently."""
     stream = torch.cuda.Stream()
     res = {}
     for name, fn in (("config2", cfg2), ("config3", cfg3), ("config4", cfg4), ("config5", cfg5),
-                     ("prefix_sweep", prefix_sweep)):
+                     ("prefix_sweep", prefix_sweep), ("tp_shares", tp_shares)):
         gen = torch.Generator(device="cuda")
         gen.manual_seed(seed)
         try:
@@ -386,5 +412,5 @@ if __name__ == "__main__":
     g = torch.Generator(device="cuda")
     g.manual_seed(2024)
     fn = {"decode_64x32k": decode_64x32k, "config2": cfg2, "config4": cfg4, "config5": cfg5,
-          "prefix_sweep": prefix_sweep}[sys.argv[1]]
+          "prefix_sweep": prefix_sweep, "tp_shares": tp_shares}[sys.argv[1]]
     print(json.dumps(fn(torch.cuda.Stream(), g)), flush=True)
