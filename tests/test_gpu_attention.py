@@ -26,6 +26,8 @@ SMALL = [
     ("varlen", [5, 0, 300, 64, 9], [33, 129, 1, 64, 0], 32, 8),
     ("g8", [0, 4000], [512, 40], 64, 8),
     ("page_edges", [15, 16, 17, 31], [1, 16, 15, 33], 8, 2),
+    ("g64_one_kv_head", [700], [40], 64, 1),
+    ("g128_one_kv_head", [300, 0], [9, 20], 128, 1),
 ]
 
 
