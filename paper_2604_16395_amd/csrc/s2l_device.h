@@ -23,14 +23,13 @@ __device__ inline uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
 }
 
-// Four E4M3 codes (one dword) -> four bf16 (two dwords).  Exact: every E4M3 value is a
-// bf16 value, and the f32 produced by v_cvt_pk_f32_fp8 has a zero low half.
+// Four E4M3 codes (one dword) -> four bf16 (two dwords), two codes per instruction
+// (v_cvt_scalef32_pk_bf16_fp8 with scale 1).  Exact: every E4M3 value is a bf16 value, so
+// the scaled conversion by 1 rounds nothing; NaN codes give bf16 NaN.
 __device__ inline u32x2 fp8x4_to_bf16x4(uint32_t w) {
-  f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
-  f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(w, true);
   u32x2 r;
-  r[0] = __builtin_amdgcn_perm(f2u(lo[1]), f2u(lo[0]), 0x07060302u);
-  r[1] = __builtin_amdgcn_perm(f2u(hi[1]), f2u(hi[0]), 0x07060302u);
+  r[0] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, false));
+  r[1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, true));
   return r;
 }
 
