@@ -22,8 +22,11 @@
 // 8-wave bf16 kernel, which runs alone on its CU; two otherwise): K(t) and V(t) are fetched
 // kStages - 1 iterations ahead of their use and each wave waits only for the copies that the
 // next step reads (vmcnt(N), N > 0), so HBM latency hides behind several tiles of MFMA
-// work.  Page ids come from scalar loads of the block table one iteration ahead.  E4M3 pages
-// go through registers and are widened to bf16 on the way (exact), with a two-stage ring.
+// work.  Page ids: each wave keeps the page of 64 consecutive tiles in one VGPR (lane l:
+// tile w0 + l; v_readlane picks a tile's), refilled from a window that an LDS-direct load
+// fetched 64 tiles earlier, so the loop issues no scalar loads (their lgkmcnt would serialise
+// the LDS operand waits).  E4M3 pages go through registers and are widened to bf16 on the way
+// (exact), with a two-stage ring.
 //
 // Compute, per wave (32 query columns, one per lane pair), per 32-key sub-block b:
 //   * S^T(b) = K Q^T with v_mfma_f32_32x32x16_bf16: A = K rows from LDS, B = Q held in
@@ -48,7 +51,9 @@
 // two MFMAs of a step's S are v_mfma_f32_32x32x64_f8f6f4 (64 dims each); P V is unchanged.
 //
 // Unsplit items write bf16 O = acc / l (and LSE).  Split items write fp32 partials
-// (acc, m, l) that split_reduce_kernel merges (log-sum-exp merge of Sec. 2.1's softmax).
+// (acc, m, l) that split_reduce_kernel merges (the standard log-sum-exp merge of partial
+// softmaxes); in the one-group bf16 layouts they are staged through LDS and stored as whole
+// rows with write-through stores.
 #include "launch.h"
 #include "plan_rules.h"
 #include "s2l_device.h"
