@@ -2,7 +2,8 @@
 // length arrays (rules in plan_rules.h, identical to the host's) and stores it at the start
 // of the caller's workspace: per-request arrays and one ItemRec per work item (so that an
 // attention workgroup finds all it needs in one scalar load).  One workgroup.  The piece
-// length comes from the host planner, which chose it from its copies of the lengths.
+// length comes from the host planner, which chose it from its copies of the lengths, and so
+// does, for the binned item order, the XCD bin of each (request, kv head) group.
 #include "launch.h"
 #include "plan_rules.h"
 
