@@ -135,6 +135,21 @@ def measure_step(layer, stream, copies, reps=5):
     return step_ms * 1e3, attn_ms * 1e3, plan
 
 
+def cfg1(stream, gen):
+    """The small single request (P = 256, C = 128, 8q/2kv, bf16 KV, 64-page pool): bound by
+    launch latency, so reported in microseconds (a fraction of the MFMA peak means nothing here)."""
+    rng = np.random.default_rng(1001)
+    P, C = np.array([256]), np.array([128])
+    layer = Layer(P, C, 8, 2, 64, tables_for(P, C, 64, rng), gen, copies=32)
+    us, attn_us, plan = measure_step(layer, stream, 32)
+    f = layer.flops()
+    return {"workload": "one request, P = 256 cached + C = 128 new, 8q/2kv, bf16 KV, 32 rotating layer copies",
+            "us_per_step": round(us, 2), "attn_us": round(attn_us, 2),
+            "attn_tflops": round(f / attn_us / 1e6, 2), "work_items": plan.num_items,
+            "tile_cols": plan.tile_cols,
+            "step": "append, plan, attention, split merge (each layer copy in turn)"}
+
+
 def cfg2(stream, gen):
     import workloads
     P, C, s = workloads.config2_lengths()
@@ -377,7 +392,7 @@ def all_configs(seed=2024):
     """{config name: result or error string}; each config is measured independently."""
     stream = torch.cuda.Stream()
     res = {}
-    for name, fn in (("config2", cfg2), ("config3", cfg3), ("config4", cfg4), ("config5", cfg5),
+    for name, fn in (("config1", cfg1), ("config2", cfg2), ("config3", cfg3), ("config4", cfg4), ("config5", cfg5),
                      ("prefix_sweep", prefix_sweep), ("tp_shares", tp_shares)):
         gen = torch.Generator(device="cuda")
         gen.manual_seed(seed)
@@ -411,6 +426,6 @@ if __name__ == "__main__":
     import sys
     g = torch.Generator(device="cuda")
     g.manual_seed(2024)
-    fn = {"decode_64x32k": decode_64x32k, "config2": cfg2, "config4": cfg4, "config5": cfg5,
+    fn = {"decode_64x32k": decode_64x32k, "config1": cfg1, "config2": cfg2, "config4": cfg4, "config5": cfg5,
           "prefix_sweep": prefix_sweep, "tp_shares": tp_shares}[sys.argv[1]]
     print(json.dumps(fn(torch.cuda.Stream(), g)), flush=True)
